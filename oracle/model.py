@@ -1,0 +1,325 @@
+"""CPU oracle: the *unmended* transformer forward, with host-side branches.
+
+Test infrastructure only.  Only the tests, the smoke check and the CPU
+baseline of the benchmark may import this package; the product never does.
+
+GraphMend rewrites a program so that it reaches exactly the result the
+original program reaches (Semantics Preservation section; fp32 outputs were
+bit-identical in the Output correctness validation paragraph).  The
+plain definition of what the mended GPU forward computes is therefore the
+original forward, in which every graph-breaking pattern is ordinary host
+control flow on a value read back from the tensor:
+
+* a validation guard ``if not C: raise`` on the inputs (Predicated Validation
+  Guards paragraph, Figure "guard_example", rule [Trap]);
+* a data-dependent ``if`` on the padding mask: ``mask.any()`` gates whether a
+  key-padding mask is applied (Data-dependent Control Flow paragraph, Figure
+  "dc_example", rule [Where]);
+* a data-dependent ``if`` on ``max(position_ids) + 1`` against the size of a
+  memoised rotary cache, whose body rebuilds the cache (the Phi-4 example of
+  the Motivation section, hoisting of a memoised initialisation in the
+  AST Transformation Pass and Semantics Preservation sections);
+* a data-dependent ``if`` on ``abs(h).max() > fp16_max - margin`` whose body
+  clamps the residual stream (rule [Where]; the untaken path must never leak
+  NaN/Inf, Semantics Preservation section);
+* print-style side effects at each taken branch, here emitted eagerly in
+  program order (rule [Defer]: the mended program replays them after the
+  graph, in FIFO order, with the values captured at the call site).
+
+All arithmetic is float64.  ``round_to`` stores a tensor in the workload's
+dtype at the storage points of the program: embedding output, norm output,
+q/k/v (after rotary), attention context, residual stream after each add,
+FFN hidden after the activation, logits.  GEMM results are never rounded
+before their epilogue (bias, activation, residual add).
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import Dict, List, Optional, Tuple
+
+import numpy as np
+
+from . import numerics as nx
+
+# Trap codes, in the order the guards appear in the program.
+TRAP_TOKEN_RANGE = 1
+TRAP_MASK_VALUE = 2
+TRAP_ROPE_CAPACITY = 3
+
+# Kinds of deferred effect records.
+EFFECT_PAD = 1
+EFFECT_REGROW = 2
+EFFECT_CLAMP = 3
+
+FP16_MAX = 65504.0
+
+
+class Trap(Exception):
+    """A validation guard failed (rule [Trap]); ``index`` is the row-major
+    position of the first offending element (0 for the rotary capacity)."""
+
+    def __init__(self, code: int, index: int):
+        super().__init__(f"trap code={code} index={index}")
+        self.code = code
+        self.index = index
+
+
+@dataclasses.dataclass
+class Effect:
+    forward: int
+    kind: int
+    layer: int
+    site: int
+    value: float
+
+
+@dataclasses.dataclass
+class OracleResult:
+    logits: np.ndarray               # storage dtype, [B, S, V]
+    logits_f64: np.ndarray           # same values as float64
+    pad_any: bool
+    regrow: bool
+    need: int
+    cached_len: int
+    clamp: List[Tuple[bool, bool]]   # per layer: (attention site, FFN site)
+    clamp_absmax: List[Tuple[float, float]]
+    clamp_nan: List[Tuple[bool, bool]]
+    clamp_margin: List[Tuple[float, float]]   # distance of max |pre-rounding| from the trip boundary
+    effects: List[Effect]
+
+
+def _cfg_get(cfg, name):
+    return getattr(cfg, name)
+
+
+class OracleModel:
+    """Float64 reference of the forward of one synthetic model.
+
+    ``weights`` is a :class:`synth.Weights` (storage-dtype arrays); layers
+    are decoded to float64 one at a time.  The rotary cache and the forward
+    counter are model state that persists across calls, as in the original
+    program (the memoised ``inv_freq``/cos/sin buffers of a rotary module).
+    """
+
+    def __init__(self, cfg, weights):
+        self.cfg = cfg
+        self.w = weights
+        self.dt = cfg.dtype
+        self.forward_count = 0
+        self.cached_len = 0
+        self.rope_cos = self.rope_sin = None
+        if cfg.pos == "rotary":
+            self._rope_build(cfg.rope_init_len)
+
+    # ---------------------------------------------------------------- helpers
+    def _g(self, name):
+        return nx.decode(self.w.globals[name], self.dt)
+
+    def _layer(self, l):
+        return {k: nx.decode(v, self.dt) for k, v in self.w.layers[l].items()}
+
+    def R(self, x):
+        return nx.round_to(x, self.dt)
+
+    def _norm(self, x, g, b):
+        c = self.cfg
+        if c.norm == "rmsnorm":
+            return nx.rms_norm(x, g, c.norm_eps)
+        return nx.layer_norm(x, g, b, c.norm_eps)
+
+    def _rope_build(self, n):
+        """Body of the rotary-cache branch: (re)build the cos/sin tables for
+        positions [0, n) and record the new cache length."""
+        self.rope_cos, self.rope_sin = nx.rope_table(
+            n, self.cfg.head_dim, self.cfg.rope_base)
+        self.cached_len = n
+
+    # ---------------------------------------------------------------- forward
+    def forward(self, ids: np.ndarray, mask: np.ndarray,
+                force: Optional[Dict] = None,
+                rows: Optional[List[int]] = None) -> OracleResult:
+        """Run the original (graph-breaking) forward.
+
+        ``force`` overrides the value a host-side predicate reads
+        (``pad_any``, ``regrow`` or ``clamp`` = {(layer, site): bool}) so that
+        each branch outcome can be exercised.  ``rows`` restricts the
+        computation to a subset of the sequences of the batch; predicates
+        that the program evaluates over the whole batch (the padding branch)
+        are still evaluated over the whole batch.  It is rejected for the
+        fp16 clamp, whose predicate reads the residual of every sequence.
+        """
+        c = self.cfg
+        force = force or {}
+        fwd = self.forward_count
+        self.forward_count += 1
+        ids = np.asarray(ids)
+        mask = np.asarray(mask)
+        B, S = ids.shape
+        assert mask.shape == (B, S)
+        effects: List[Effect] = []
+
+        # --- validation guards on the inputs (rule [Trap]), program order.
+        bad = (ids < 0) | (ids >= c.vocab)
+        if bad.any():
+            raise Trap(TRAP_TOKEN_RANGE, int(np.argmax(bad.reshape(-1))))
+        bad = (mask != 0) & (mask != 1)
+        if bad.any():
+            raise Trap(TRAP_MASK_VALUE, int(np.argmax(bad.reshape(-1))))
+
+        # --- padding branch: a data-dependent if on the mask (host read).
+        pad_any = bool((mask == 0).any())
+        if "pad_any" in force:
+            pad_any = bool(force["pad_any"])
+        if pad_any:
+            effects.append(Effect(fwd, EFFECT_PAD, -1, -1,
+                                  float((mask == 0).sum())))
+
+        # --- rotary cache branch: seq_len read back from max(position_ids).
+        positions = np.broadcast_to(np.arange(S), (B, S))
+        need = int(positions.max()) + 1
+        regrow = False
+        if c.pos == "rotary":
+            if need > c.rope_capacity:
+                raise Trap(TRAP_ROPE_CAPACITY, 0)
+            regrow = need > self.cached_len
+            if "regrow" in force:
+                regrow = bool(force["regrow"])
+            if regrow:
+                self._rope_build(need)
+                effects.append(Effect(fwd, EFFECT_REGROW, -1, -1, float(need)))
+            if need > self.cached_len:
+                # The original program indexes the cache past its end.
+                raise IndexError(
+                    f"rotary cache holds {self.cached_len} positions, {need} needed")
+
+        if rows is None:
+            rows = list(range(B))
+        if c.fp16_clamp and len(rows) != B:
+            raise ValueError("the clamp predicate needs every sequence")
+        ids_r = ids[rows]
+        mask_r = mask[rows]
+        Br = len(rows)
+
+        # --- attention mask: causal and/or key padding (only if pad_any).
+        allowed = np.ones((Br, 1, S, S), dtype=bool)
+        if c.causal:
+            allowed &= np.tril(np.ones((S, S), dtype=bool))[None, None]
+        if pad_any:
+            allowed &= (mask_r == 1)[:, None, None, :]
+
+        # --- embedding.
+        x = self._g("tok_emb")[ids_r]
+        if c.pos == "learned":
+            x = x + self._g("pos_emb")[:S][None]
+        h = self.R(x)
+        if c.emb_norm:
+            h = self.R(self._norm(h, self._g("emb_ln_g"),
+                                  self._g("emb_ln_b") if c.norm == "layernorm" else None))
+
+        clamp, absmaxes, nans, margins = [], [], [], []
+        d, H, hd = c.d_model, c.n_heads, c.head_dim
+        for l in range(c.n_layers):
+            W = self._layer(l)
+            site_out = []
+            # ---------------- attention block
+            a = self.R(self._norm(h, W["ln1_g"], W.get("ln1_b"))) if c.norm_place == "pre" else h
+            qkv = a @ W["wqkv"].T
+            if c.bias:
+                qkv = qkv + W["bqkv"]
+            q = qkv[..., :d].reshape(Br, S, H, hd).transpose(0, 2, 1, 3)
+            k = qkv[..., d:2 * d].reshape(Br, S, H, hd).transpose(0, 2, 1, 3)
+            v = qkv[..., 2 * d:].reshape(Br, S, H, hd).transpose(0, 2, 1, 3)
+            if c.pos == "rotary":
+                cos = self.rope_cos[:S]
+                sin = self.rope_sin[:S]
+                q = nx.apply_rope(q, cos, sin)
+                k = nx.apply_rope(k, cos, sin)
+            q, k, v = self.R(q), self.R(k), self.R(v)
+            s = (q @ k.transpose(0, 1, 3, 2)) * (1.0 / np.sqrt(hd))
+            p = nx.masked_softmax(s, allowed)
+            ctx = self.R(p @ v).transpose(0, 2, 1, 3).reshape(Br, S, d)
+            o = ctx @ W["wo"].T
+            if c.bias:
+                o = o + W["bo"]
+            pre = h + o
+            h = self.R(pre)
+            if c.norm_place == "post":
+                h = self.R(self._norm(h, W["ln1_g"], W.get("ln1_b")))
+            h, info = self._clamp_site(h, pre, l, 0, force, fwd, effects)
+            site_out.append(info)
+
+            # ---------------- feed-forward block
+            a = self.R(self._norm(h, W["ln2_g"], W.get("ln2_b"))) if c.norm_place == "pre" else h
+            u = a @ W["w1"].T
+            if c.bias:
+                u = u + W["b1"]
+            if c.gated:
+                ff = c.d_ff
+                g_, up = u[..., :ff], u[..., ff:]
+                act = nx.gelu(g_) if c.ffn == "geglu" else nx.silu(g_)
+                f = self.R(act * up)
+            else:
+                f = self.R(nx.gelu(u))
+            y = f @ W["w2"].T
+            if c.bias:
+                y = y + W["b2"]
+            pre = h + y
+            h = self.R(pre)
+            if c.norm_place == "post":
+                h = self.R(self._norm(h, W["ln2_g"], W.get("ln2_b")))
+            h, info = self._clamp_site(h, pre, l, 1, force, fwd, effects)
+            site_out.append(info)
+            clamp.append((site_out[0][0], site_out[1][0]))
+            absmaxes.append((site_out[0][1], site_out[1][1]))
+            nans.append((site_out[0][2], site_out[1][2]))
+            margins.append((site_out[0][3], site_out[1][3]))
+
+        # --- head.
+        if c.norm_place == "pre":
+            z = self.R(self._norm(h, self._g("lnf_g"),
+                                  self._g("lnf_b") if c.norm == "layernorm" else None))
+        else:
+            z = h
+        head = self._g("tok_emb") if c.tied_head else self._g("lm_head")
+        logits = self.R(z @ head.T)
+        return OracleResult(
+            logits=nx.to_storage(logits, self.dt), logits_f64=logits,
+            pad_any=pad_any, regrow=regrow, need=need,
+            cached_len=self.cached_len, clamp=clamp, clamp_absmax=absmaxes,
+            clamp_nan=nans, clamp_margin=margins, effects=effects)
+
+    def _clamp_site(self, h, pre, l, s, force, fwd, effects):
+        """fp16 overflow guard after a residual add: ``if abs(h).max() >
+        fp16_max - margin: h = clamp(h)``.  ``max`` propagates NaN, and
+        ``NaN > thr`` is False, so a NaN anywhere leaves h unclamped."""
+        c = self.cfg
+        if not c.fp16_clamp:
+            return h, (False, 0.0, False, float("inf"))
+        thr = FP16_MAX - c.clamp_margin
+        has_nan = bool(np.isnan(h).any())
+        m = float(np.abs(h).max()) if not has_nan else float("nan")
+        trip = (not has_nan) and m > thr
+        # distance of the largest pre-rounding magnitude from the value at
+        # which the stored fp16 value first exceeds thr.
+        boundary = _fp16_trip_boundary(thr)
+        with np.errstate(invalid="ignore"):
+            pm = float(np.nanmax(np.abs(pre)))
+        margin = abs(pm - boundary)
+        if (l, s) in force.get("clamp", {}):
+            trip = bool(force["clamp"][(l, s)])
+        if trip:
+            lim = thr
+            h = self.R(np.clip(h, -lim, lim))
+            effects.append(Effect(fwd, EFFECT_CLAMP, l, s, m))
+        absmax = m if not has_nan else float(np.abs(h[~np.isnan(h)]).max(initial=0.0))
+        return h, (trip, absmax, has_nan, margin)
+
+
+def _fp16_trip_boundary(thr: float) -> float:
+    """Smallest magnitude whose fp16 rounding exceeds ``thr``: the midpoint
+    between the largest fp16 value <= thr and the next fp16 value."""
+    lo = np.float16(thr)
+    if float(lo) > thr:
+        lo = np.nextafter(lo, np.float16(0))
+    hi = np.nextafter(lo, np.float16(np.inf))
+    return (float(lo) + float(hi)) / 2.0
