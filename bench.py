@@ -1,0 +1,171 @@
+#!/usr/bin/env python3
+"""Steady-state forward throughput of libgm on one MI355X.
+
+Workload: the 12-layer causal LM decoder (d_model 768, 12 heads, FFN 3072
+GELU, pre-LayerNorm, learned positions, vocab 50257, bf16) over a batch of
+8 x 512 tokens with 0..128 trailing pads per sequence (synthetic weights
+N(0, 0.02), uniform token ids).  One step = one gm_forward: a single
+hipGraphLaunch of the whole forward, every data-dependent branch (padding
+mask, guards, effects) resolved on the device.
+
+Prints one JSON line with the throughput, the host syncs per forward (from
+the library's counters), a roofline entry for the dominant kernel (the MFMA
+GEMM) measured with HIP events on the launch stream, and the CPU oracle
+timed on a bounded sample of the same workload.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+WORKLOAD = "causal_lm_768"
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(cfg, w, ids, mask, rows):
+    """The oracle (float64 NumPy) on `rows` sequences of the same batch."""
+    import numpy as np
+    from oracle import OracleModel
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    m = OracleModel(cfg, w)
+    t0 = time.perf_counter()
+    m.forward(ids, mask, rows=rows)
+    dt = time.perf_counter() - t0
+    tokens = len(rows) * ids.shape[1]
+    return {"value": tokens / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{len(rows)} of {ids.shape[0]} sequences x {ids.shape[1]} tokens "
+                      f"(full 12-layer forward + LM head), {dt:.2f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=2)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on exactly one GPU (got --gpus {args.gpus}); "
+              "the multi-GPU layout is described in DESIGN.md, not built", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2509_16248_amd.model import GmModel
+
+    cfg = synth.preset(WORKLOAD)
+    B, S = cfg.batch, cfg.seq
+    log(f"[bench] generating weights for {WORKLOAD}")
+    w = synth.make_weights(cfg, 1234)
+    ids, mask = synth.make_inputs(cfg, 0)
+    m = GmModel(cfg, w.globals, w.layers, device="cuda:0")
+    ids_t = torch.from_numpy(ids).cuda()
+    mask_t = torch.from_numpy(mask).cuda()
+    out = m.new_logits(B, S)
+    stream = torch.cuda.current_stream()
+
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    m.forward(ids_t, mask_t, out)
+    torch.cuda.synchronize()
+    cold_ms = (time.perf_counter() - t0) * 1e3
+    log(f"[bench] cold forward (capture + instantiate + run) {cold_ms:.2f} ms")
+    for _ in range(args.warmup):
+        m.forward(ids_t, mask_t, out)
+    torch.cuda.synchronize()
+    s0 = m.stats()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        m.forward(ids_t, mask_t, out)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / args.steps
+    s1 = m.stats()
+    syncs = (s1["host_syncs_in_forward"] - s0["host_syncs_in_forward"]) / args.steps
+    launches = (s1["graph_launches"] - s0["graph_launches"]) / args.steps
+    log(f"[bench] {ms:.4f} ms/forward, graph launches/forward {launches}, "
+        f"host syncs/forward {syncs}, kernels/forward {s1['kernels_per_forward']}")
+
+    # per-kernel durations: eager forwards with events between the kernels
+    prof = None
+    for _ in range(3):
+        prof = m.profile(ids_t, mask_t, out)
+    by_kind = {}
+    for kind, layer, kms, flops, nbytes in prof:
+        t = by_kind.setdefault(kind, [0, 0.0, 0.0, 0.0])
+        t[0] += 1
+        t[1] += kms
+        t[2] += flops
+        t[3] += nbytes
+    gemm = [p for p in prof if p[0].startswith("gemm")]
+    g_ms = sum(p[2] for p in gemm)
+    g_flops = sum(p[3] for p in gemm)
+    g_avg_ms = g_ms / len(gemm)
+    achieved = g_flops / (g_ms * 1e-3) / 1e12
+    roofline = {"kernel": "k_gemm_mfma<bf16> (all projection and LM-head GEMMs)",
+                "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                "traffic": None, "launches_per_forward": len(gemm),
+                "avg_launch_ms": round(g_avg_ms, 5),
+                "flops_per_launch_avg": g_flops / len(gemm)}
+    breakdown = {k: {"launches": v[0], "ms": round(v[1], 4),
+                     "tflops": round(v[2] / (v[1] * 1e-3) / 1e12, 2) if v[2] else None,
+                     "gbs": round(v[3] / (v[1] * 1e-3) / 1e9, 1) if v[3] and not v[2] else None}
+                 for k, v in by_kind.items()}
+    log(f"[bench] kernel breakdown (eager, ms): " +
+        ", ".join(f"{k}={v['ms']}" for k, v in breakdown.items()))
+
+    result = {
+        "metric": "steady-state forward tokens/sec + host syncs/forward (must be 0), 1 MI355X",
+        "value": round(B * S / (ms * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "causal_lm_768: 12-layer causal LM decoder, d_model 768, "
+                               "12 heads, FFN 3072 GELU, pre-LayerNorm, learned positions, "
+                               "vocab 50257, bf16, weights N(0,0.02)",
+                   "global_batch": B, "seq_len": S,
+                   "pad_tokens": int((mask == 0).sum()), "parallelism": "single GPU"},
+        "host_syncs_per_forward": syncs,
+        "graph_launches_per_forward": launches,
+        "kernels_per_forward": s1["kernels_per_forward"],
+        "cold_ms": round(cold_ms, 2),
+        "nonpad_tokens_per_s": round(int(mask.sum()) / (ms * 1e-3), 1),
+        "roofline": roofline,
+        "kernel_breakdown_eager_ms": breakdown,
+    }
+    m.close()
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a sample")
+        result["cpu_baseline"] = cpu_baseline(cfg, w, ids, mask, list(range(args.cpu_rows)))
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,250 @@
+/*
+ * gm.h -- C ABI of libgm: a transformer decoder/encoder forward for MI355X
+ * (gfx950) in which every graph-breaking pattern is resolved on the device.
+ *
+ * The operation.  GraphMend ("Code Transformations for Fixing Graph Breaks in
+ * PyTorch 2") rewrites three source patterns so that a model forward stays in
+ * one captured graph: a validation guard `if not C: raise` becomes an
+ * asynchronous device assertion (rule [Trap]); a tensor-predicated if/else
+ * becomes both branches plus a select (rule [Where]); print/logger calls are
+ * recorded with their arguments and replayed after the graph (rule [Defer])
+ * (Table "GraphMend transformation rules"; Semantics Preservation section).
+ * This library is the forward those rewrites produce, written directly for
+ * the GPU: the guards on the inputs, the `mask.any()` padding branch, the
+ * rotary-cache regrow on sequence length and the fp16 `abs().max()` overflow
+ * clamp are device reductions that feed flags read by later kernels, so the
+ * host never reads a value back during a forward.  Each forward is one
+ * hipGraphLaunch on the caller's stream.
+ *
+ * Conventions.
+ *  - Every pointer marked "device" is a HIP device pointer on the device that
+ *    was current when the model was created.  Every pointer marked "host" is
+ *    ordinary host memory.
+ *  - Every function returns GM_OK (0) or a negative GM_E_* code.  Errors that
+ *    depend on input *values* (token range, mask values, rotary capacity) are
+ *    never returned by gm_forward (that would need a host sync): they set the
+ *    model's sticky device trap word, read with gm_check_error (rule [Trap]:
+ *    the failure surfaces at the next synchronisation point).
+ *  - A model is used from one host thread and one stream at a time.
+ */
+#ifndef GM_H_
+#define GM_H_
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define GM_ABI_VERSION 1
+#define GM_MAX_LAYERS 64
+
+/* ------------------------------------------------------------ return codes */
+#define GM_OK          0
+#define GM_E_INVAL    -1  /* null pointer, bad shape, unsupported combination */
+#define GM_E_NOMEM    -2  /* device allocation failed (gm_model_create only)  */
+#define GM_E_HIP      -3  /* a HIP runtime call failed; see gm_last_error     */
+#define GM_E_CAPTURE  -4  /* graph capture or instantiation failed            */
+
+/* ------------------------------------------------------------ enums */
+enum { GM_DTYPE_F32 = 0, GM_DTYPE_BF16 = 1, GM_DTYPE_F16 = 2 };
+enum { GM_NORM_LAYER = 0, GM_NORM_RMS = 1 };
+enum { GM_NORM_PRE = 0, GM_NORM_POST = 1 };
+enum { GM_FFN_GELU = 0, GM_FFN_GEGLU = 1, GM_FFN_SWIGLU = 2 };
+enum { GM_POS_NONE = 0, GM_POS_LEARNED = 1, GM_POS_ROTARY = 2 };
+
+/* Trap codes, in the order the guards run (smaller code = earlier guard). */
+enum { GM_TRAP_NONE = 0, GM_TRAP_TOKEN_RANGE = 1, GM_TRAP_MASK_VALUE = 2,
+       GM_TRAP_ROPE_CAPACITY = 3 };
+
+/* Kinds of deferred effect records (rule [Defer]). */
+enum { GM_EFFECT_PAD = 1, GM_EFFECT_REGROW = 2, GM_EFFECT_CLAMP = 3 };
+
+/* ------------------------------------------------------------ config
+ * Model hyper-parameters.  Read only during gm_model_create.
+ *  d_model % n_heads == 0; head_dim = d_model / n_heads must be 32, 64 or
+ *  128; for bf16/f16 d_model and d_ff must be multiples of 64.
+ *  act_dtype is the storage dtype of weights, activations and logits; all
+ *  accumulation is fp32.
+ *  norm_place POST applies the norm after each residual add (no final norm);
+ *  PRE applies it before each block and once before the head.
+ *  emb_norm applies a norm (emb_ln_g/emb_ln_b) to the embedding output.
+ *  Rotary: cos/sin table of rope_capacity rows, the first rope_init_len rows
+ *  built at create; a forward that needs more rows (max position + 1 >
+ *  cached length) grows it on the device to exactly that length.
+ *  fp16_clamp (f16 + PRE only): after each residual add, if no element is
+ *  NaN and max |h| > 65504 - clamp_margin, h is clamped to that bound.
+ */
+typedef struct gm_config {
+  int32_t abi_version;      /* must be GM_ABI_VERSION */
+  int32_t n_layers, d_model, n_heads, d_ff, vocab;
+  int32_t max_batch, max_seq;
+  int32_t norm, norm_place, emb_norm, ffn, pos, causal, has_bias, tied_head;
+  float   norm_eps;
+  float   rope_base;
+  int32_t rope_init_len, rope_capacity;
+  int32_t act_dtype;
+  int32_t fp16_clamp;
+  float   clamp_margin;
+} gm_config;
+
+/* ------------------------------------------------------------ weights
+ * Device pointers in PyTorch nn.Linear layout (weight [out, in], row-major),
+ * dtype act_dtype.  Pointers that the config does not use must be NULL.
+ *  wqkv [3d, d]  rows: q (d), k (d), v (d); bqkv [3d]
+ *  wo   [d, d];  bo [d]
+ *  w1   [ff, d] (GELU) or [2ff, d] (gated: gate rows first, then up rows); b1
+ *  w2   [d, ff]; b2 [d]
+ *  ln*_g / ln*_b [d] (b only for LayerNorm)
+ *  tok_emb [vocab, d]; pos_emb [max_seq, d] (learned positions)
+ *  lm_head [vocab, d] (NULL when tied_head: the head is tok_emb)
+ * The library copies (and repacks) everything during gm_model_create; the
+ * caller may free its buffers when that call returns.
+ */
+typedef struct gm_layer_weights {
+  const void *ln1_g, *ln1_b, *wqkv, *bqkv, *wo, *bo;
+  const void *ln2_g, *ln2_b, *w1, *b1, *w2, *b2;
+} gm_layer_weights;
+
+typedef struct gm_weights {
+  const void *tok_emb, *pos_emb, *emb_ln_g, *emb_ln_b, *lnf_g, *lnf_b, *lm_head;
+  const gm_layer_weights *layers;   /* host array of n_layers entries */
+} gm_weights;
+
+typedef struct gm_model gm_model;
+
+/* Decisions of the last completed forward (the device predicates). */
+typedef struct gm_decisions {
+  int32_t pad_any;        /* mask had a 0 -> key-padding mask applied        */
+  int32_t regrow;         /* rotary table grown in this forward              */
+  int32_t need;           /* max(position) + 1                               */
+  int32_t cached_len;     /* rotary rows valid after this forward (state)    */
+  int32_t n_clamp_sites;  /* 2 * n_layers with fp16_clamp, else 0            */
+  int32_t clamp[2 * GM_MAX_LAYERS];        /* site 2l: after attention, 2l+1: after FFN */
+  float   clamp_absmax[2 * GM_MAX_LAYERS]; /* max |h| over non-NaN elements */
+  int32_t clamp_nan[2 * GM_MAX_LAYERS];    /* some element of h was NaN     */
+  int32_t forward_index;  /* 0-based count of forwards enqueued before it     */
+} gm_decisions;
+
+/* One deferred effect: what the original program would have printed. */
+typedef struct gm_effect {
+  int32_t forward;   /* forward_index of the forward that recorded it */
+  int32_t kind;      /* GM_EFFECT_*                                   */
+  int32_t layer;     /* clamp: layer; otherwise -1                    */
+  int32_t site;      /* clamp: 0 attention, 1 FFN; otherwise -1       */
+  float   value;     /* pad: #pad positions; regrow: need; clamp: max |h| */
+} gm_effect;
+
+typedef void (*gm_effect_cb)(const gm_effect *effect, void *user);
+
+/* Kernel kinds reported by gm_profile_forward. */
+enum { GM_K_PROLOGUE = 0, GM_K_ROPE = 1, GM_K_EMBED = 2, GM_K_NORM = 3,
+       GM_K_GEMM_QKV = 4, GM_K_ATTENTION = 5, GM_K_GEMM_O = 6, GM_K_GEMM_UP = 7,
+       GM_K_GEMM_DOWN = 8, GM_K_GEMM_HEAD = 9, GM_K_EFFECTS = 10 };
+
+/* One kernel launch of a profiled forward.  flops/bytes are the launch's
+ * algorithmic work (2*M*N*K for a GEMM; 4*hd*visible (query,key) pairs per
+ * head for attention; bytes read + written once for the others). */
+typedef struct gm_kernel_time {
+  int32_t kind;      /* GM_K_*                                  */
+  int32_t layer;     /* layer index, -1 outside the layer stack */
+  float   ms;        /* duration between the events around it   */
+  double  flops;
+  double  bytes;
+} gm_kernel_time;
+
+typedef struct gm_stats {
+  uint64_t forwards;         /* gm_forward / gm_forward_ex calls              */
+  uint64_t captures;         /* graphs captured (cold calls)                  */
+  uint64_t graph_launches;   /* hipGraphLaunch calls                          */
+  uint64_t eager_forwards;   /* forwards enqueued without a graph             */
+  uint64_t host_syncs_in_forward; /* sync-class HIP calls made inside a forward */
+  uint64_t kernels_per_forward;   /* kernel nodes in the last captured graph  */
+} gm_stats;
+
+/* ------------------------------------------------------------ entry points */
+
+/* Create a model on the current device: validate cfg (host checks of shapes
+ * and dtypes, the static half of [Trap]), allocate weights, workspace for
+ * max_batch x max_seq tokens and device state, copy and repack the weights,
+ * build rotary rows [0, rope_init_len).  Synchronous.  On success *out owns
+ * all of it; free with gm_model_destroy.  Returns GM_E_INVAL, GM_E_NOMEM or
+ * GM_E_HIP on failure (*out is then NULL). */
+int gm_model_create(const gm_config *cfg, const gm_weights *w, gm_model **out);
+
+/* Release everything the model owns.  Synchronises the device first.  NULL
+ * is ignored. */
+void gm_model_destroy(gm_model *m);
+
+/* Enqueue one forward over [max_batch, max_seq] tokens on `stream`.
+ *  token_ids  device int32 [B, S] row-major, each in [0, vocab)
+ *  attn_mask  device int32 [B, S] row-major, 1 = token, 0 = padding
+ *  out_logits device [B, S, vocab] in act_dtype, row-major
+ * Asynchronous: no host synchronisation, no device-to-host copy and no
+ * allocation once the (B, S, pointers) combination has been seen; the first
+ * call with a new combination captures and instantiates a graph (cold
+ * start).  The buffers must stay valid until the stream reaches the end of
+ * the forward.  Value errors go to the trap word (gm_check_error); the
+ * logits of a trapped forward are unspecified but every access stays in
+ * bounds. */
+int gm_forward(gm_model *m, const int32_t *token_ids, const int32_t *attn_mask,
+               void *out_logits, hipStream_t stream);
+
+/* As gm_forward over B <= max_batch sequences of S <= max_seq tokens. */
+int gm_forward_ex(gm_model *m, int32_t B, int32_t S, const int32_t *token_ids,
+                  const int32_t *attn_mask, void *out_logits, hipStream_t stream);
+
+/* Run one forward without a graph, recording a HIP event on `stream` after
+ * every kernel, wait for it, and write one gm_kernel_time per launch (in
+ * launch order) to out[0 .. min(cap, *n_out)).  Same kernels and results as
+ * gm_forward_ex; synchronises `stream`, so it is a profiling call, not a
+ * hot-path one. */
+int gm_profile_forward(gm_model *m, int32_t B, int32_t S, const int32_t *token_ids,
+                       const int32_t *attn_mask, void *out_logits, hipStream_t stream,
+                       gm_kernel_time *out, int32_t cap, int32_t *n_out);
+
+/* Use one captured hipGraph per forward (enabled = 1, the default) or
+ * enqueue the kernels one by one (enabled = 0; same kernels, same results). */
+int gm_set_graph_mode(gm_model *m, int32_t enabled);
+
+/* Copy the decisions of the last forward enqueued on `stream` into *out.
+ * Synchronises `stream`; not for use inside a timed loop. */
+int gm_read_decisions(gm_model *m, gm_decisions *out, hipStream_t stream);
+
+/* Device address of the model's int32 decision slots, for zero-sync reads by
+ * later kernels: [0] pad_any, [1] regrow, [2] need, [3] cached_len. */
+const int32_t *gm_decisions_device_ptr(const gm_model *m);
+
+/* Return and clear the sticky trap word: *code = GM_TRAP_* of the first
+ * failing guard of the first trapped forward since the last call, *index =
+ * row-major position of the first offending element (0 for the rotary
+ * capacity).  Synchronises the device. */
+int gm_check_error(gm_model *m, int32_t *code, int32_t *index);
+
+/* Replay the deferred effect records in FIFO order through cb (which may be
+ * NULL to discard them) and empty the buffer.  *n_dropped (may be NULL)
+ * receives the number of records lost to overflow since the last flush.
+ * Synchronises the device. */
+int gm_flush_effects(gm_model *m, gm_effect_cb cb, void *user, int32_t *n_dropped);
+
+/* Device address and size in bytes of an internal activation buffer, for
+ * inspection after the stream has completed a forward (debugging and
+ * tests).  which: 0 residual stream h [T, d], 1 norm output [T, d],
+ * 2 fused q|k|v [T, 3d], 3 attention context [T, d], 4 FFN hidden [T, d_ff]
+ * (T = max_batch * max_seq rows, act_dtype).  Contents are those left by the
+ * last kernel that wrote the buffer. */
+int gm_debug_buffer(const gm_model *m, int32_t which, void **ptr, uint64_t *bytes);
+
+/* Host counters (no device access). */
+int gm_get_stats(const gm_model *m, gm_stats *out);
+
+/* Static description of a return code, and the last HIP error message of
+ * the calling thread. */
+const char *gm_strerror(int code);
+const char *gm_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* GM_H_ */

@@ -1,0 +1,346 @@
+// gm_gemm.hip -- out = epilogue(A . W^T) for the projections and the head.
+//
+// A is [M, K] (activations, row-major), W is [N, K] (nn.Linear weight
+// layout, row-major): both operands are contiguous along K, which is the
+// operand layout the matrix cores read.  bf16/fp16 run on gfx950 MFMA
+// (v_mfma_f32_16x16x32_{bf16,f16}) with fp32 accumulation; fp32 runs on a
+// plain LDS-tiled FMA kernel.  All epilogues work on fp32 accumulators and
+// round once to the storage dtype.
+#include <math.h>
+
+#include "gm_device.h"
+#include "gm_kernels.h"
+
+namespace gm {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+template <typename T> struct Mfma;
+template <> struct Mfma<bf16_t> {
+  typedef bf16x8 vec;
+  static __device__ __forceinline__ f32x4 run(vec a, vec b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+  }
+};
+template <> struct Mfma<f16_t> {
+  typedef f16x8 vec;
+  static __device__ __forceinline__ f32x4 run(vec a, vec b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+  }
+};
+
+// ------------------------------------------------------------ epilogue
+template <typename T>
+__device__ __forceinline__ void load4(const T* p, float* v, int nvalid, bool vec) {
+  if (vec) {
+    if constexpr (sizeof(T) == 4) {
+      const float4 r = *reinterpret_cast<const float4*>(p);
+      v[0] = r.x; v[1] = r.y; v[2] = r.z; v[3] = r.w;
+    } else {
+      const uint2 r = *reinterpret_cast<const uint2*>(p);
+      const T* e = reinterpret_cast<const T*>(&r);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] = to_f32(e[i]);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = i < nvalid ? to_f32(p[i]) : 0.f;
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ void store4(T* p, const float* v, int nvalid, bool vec) {
+  if (vec) {
+    if constexpr (sizeof(T) == 4) {
+      *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+    } else {
+      uint2 r;
+      T* e = reinterpret_cast<T*>(&r);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) e[i] = from_f32<T>(v[i]);
+      *reinterpret_cast<uint2*>(p) = r;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (i < nvalid) p[i] = from_f32<T>(v[i]);
+  }
+}
+
+__device__ __forceinline__ float gelu_f(float x) {
+  return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f));
+}
+__device__ __forceinline__ float silu_f(float x) { return x / (1.0f + expf(-x)); }
+
+struct SiteMax {
+  uint32_t amax = 0;
+  int nan = 0;
+  __device__ __forceinline__ void add(float y) {
+    if (y != y) nan = 1;
+    else {
+      const uint32_t u = __float_as_uint(y) & 0x7FFFFFFFu;
+      amax = u > amax ? u : amax;
+    }
+  }
+};
+
+// Four consecutive packed columns nA..nA+3 (first tile of a pair, values
+// va) and nA+16..nA+19 (second tile, values vb) of output row m.
+template <typename T>
+__device__ __forceinline__ void epi_pair(const GemmArgs& a, int m, int nA,
+                                         const float* va, const float* vb,
+                                         SiteMax& sm) {
+  if (m >= a.M) return;
+  const T* bias = static_cast<const T*>(a.bias);
+  T* out = static_cast<T*>(a.out);
+  const long long orow = static_cast<long long>(m) * a.ldo;
+  if (a.epi == kEpiGatedGelu || a.epi == kEpiGatedSilu) {
+    const int jo = (nA >> 5) * 16 + (nA & 15);
+    float y[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float g = va[r], u = vb[r];
+      if (bias) {
+        g += to_f32(bias[nA + r]);
+        u += to_f32(bias[nA + 16 + r]);
+      }
+      const float act = a.epi == kEpiGatedGelu ? gelu_f(g) : silu_f(g);
+      y[r] = act * u;
+    }
+    store4(out + orow + jo, y, 4, (a.ldo & 3) == 0);
+    return;
+  }
+  if (a.epi == kEpiRope && nA < 2 * a.d_model) {
+    const int d = a.d_model, hd = a.head_dim, P = hd >> 1;
+    const int region = nA >= d;
+    const int nr = nA - region * d;
+    const int h = nr / hd, within = nr - h * hd;
+    const int i = (within >> 5) * 16 + (within & 15);
+    int pos = m % a.seq;
+    pos = pos < a.rope_rows ? pos : a.rope_rows - 1;
+    const float* cs = a.rope_cos + static_cast<long long>(pos) * P + i;
+    const float* sn = a.rope_sin + static_cast<long long>(pos) * P + i;
+    float o1[4], o2[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float x1 = va[r], x2 = vb[r];
+      if (bias) {
+        x1 += to_f32(bias[nA + r]);
+        x2 += to_f32(bias[nA + 16 + r]);
+      }
+      o1[r] = x1 * cs[r] - x2 * sn[r];
+      o2[r] = x2 * cs[r] + x1 * sn[r];
+    }
+    const long long base = orow + region * d + h * hd + i;
+    const bool vec = (a.ldo & 3) == 0;
+    store4(out + base, o1, 4, vec);
+    store4(out + base + P, o2, 4, vec);
+    return;
+  }
+  // independent columns: store / gelu / residual (and v of kEpiRope)
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int n0 = nA + 16 * t;
+    if (n0 >= a.N) continue;
+    const float* v = t ? vb : va;
+    const int nvalid = a.N - n0 < 4 ? a.N - n0 : 4;
+    const bool vec = nvalid == 4 && (a.ldo & 3) == 0;
+    float y[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) y[r] = v[r];
+    if (bias)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        if (r < nvalid) y[r] += to_f32(bias[n0 + r]);
+    if (a.epi == kEpiGelu)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) y[r] = gelu_f(y[r]);
+    if (a.epi == kEpiResid) {
+      float rv[4];
+      load4(static_cast<const T*>(a.resid) + static_cast<long long>(m) * a.ldr + n0, rv,
+            nvalid, nvalid == 4 && (a.ldr & 3) == 0);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) y[r] += rv[r];
+      if (a.site >= 0)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (r < nvalid) sm.add(round_as<T>(y[r]));
+    }
+    store4(out + orow + n0, y, nvalid, vec);
+  }
+}
+
+__device__ __forceinline__ void site_flush(const GemmArgs& a, SiteMax& sm) {
+  if (a.site < 0) return;
+  const uint32_t m = wave_max_u32(sm.amax);
+  const int n = wave_or(sm.nan);
+  if ((threadIdx.x & 63) == 0) {
+    if (m) atomicMax(reinterpret_cast<unsigned int*>(a.state + kAbsmaxBase + a.site), m);
+    if (n) atomicOr(a.state + kNanBase + a.site, 1);
+  }
+}
+
+// ------------------------------------------------------------ MFMA kernel
+// Workgroup tile 128 x 128, K step 64, 4 wavefronts in a 2 x 2 grid, each
+// wavefront 64 x 64 = 4 x 4 MFMA tiles of 16 x 16.  W is the MFMA A operand
+// and A the B operand, so each lane ends up with 4 consecutive output
+// columns of one row (vector stores, pair epilogues in registers).
+// Operand tiles are staged in LDS with a 16-byte row pad; the next K step is
+// prefetched into registers while the current one is multiplied.
+constexpr int kBM = 128, kBN = 128, kBK = 64, kLDK = kBK + 8;
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_gemm_mfma(GemmArgs a) {
+  typedef typename Mfma<T>::vec vec;
+  __shared__ __attribute__((aligned(16))) T sA[2][kBM * kLDK];
+  __shared__ __attribute__((aligned(16))) T sB[2][kBN * kLDK];
+  const int tiles_n = (a.N + kBN - 1) / kBN;
+  const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
+  const int bm = tm * kBM, bn = tn * kBN;
+  const int t = threadIdx.x;
+  const int lrow = t >> 3, lcol = (t & 7) * 8;
+  const T* Ag[4];
+  const T* Wg[4];
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    int r = bm + lrow + 32 * v;
+    r = r < a.M ? r : a.M - 1;
+    Ag[v] = static_cast<const T*>(a.A) + static_cast<long long>(r) * a.lda + lcol;
+    int c = bn + lrow + 32 * v;
+    c = c < a.N ? c : a.N - 1;
+    Wg[v] = static_cast<const T*>(a.W) + static_cast<long long>(c) * a.ldw + lcol;
+  }
+  uint4 ra[4], rb[4];
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      ra[v] = *reinterpret_cast<const uint4*>(Ag[v] + k0);
+      rb[v] = *reinterpret_cast<const uint4*>(Wg[v] + k0);
+    }
+  };
+  auto sstore = [&](int buf) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      *reinterpret_cast<uint4*>(&sA[buf][(lrow + 32 * v) * kLDK + lcol]) = ra[v];
+      *reinterpret_cast<uint4*>(&sB[buf][(lrow + 32 * v) * kLDK + lcol]) = rb[v];
+    }
+  };
+  const int wave = t >> 6, lane = t & 63;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int l16 = lane & 15, g = lane >> 4;
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int nk = a.K / kBK;
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < nk) gload((kt + 1) * kBK);
+#pragma unroll
+    for (int kc = 0; kc < 2; ++kc) {
+      vec af[4], bfr[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        af[i] = *reinterpret_cast<const vec*>(
+            &sA[buf][(wm * 64 + 16 * i + l16) * kLDK + kc * 32 + g * 8]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        bfr[j] = *reinterpret_cast<const vec*>(
+            &sB[buf][(wn * 64 + 16 * j + l16) * kLDK + kc * 32 + g * 8]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = Mfma<T>::run(bfr[j], af[i], acc[i][j]);
+    }
+    if (kt + 1 < nk) sstore(buf ^ 1);
+    __syncthreads();
+  }
+
+  SiteMax sm;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int m = bm + wm * 64 + 16 * i + l16;
+#pragma unroll
+    for (int j = 0; j < 4; j += 2) {
+      const int nA = bn + wn * 64 + 16 * j + 4 * g;
+      float va[4], vb[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        va[r] = acc[i][j][r];
+        vb[r] = acc[i][j + 1][r];
+      }
+      epi_pair<T>(a, m, nA, va, vb, sm);
+    }
+  }
+  site_flush(a, sm);
+}
+
+// ------------------------------------------------------------ fp32 kernel
+// 64 x 64 tile, K step 16; thread t owns row t/4 and, in each of the four
+// 16-column groups, the 4 consecutive columns 4*(t%4).. (same pairing of
+// 16-column groups as the MFMA kernel, so the epilogue is shared).
+template <typename T>
+__global__ __launch_bounds__(256) void k_gemm_simple(GemmArgs a) {
+  __shared__ float sA[64][17];
+  __shared__ float sB[64][17];
+  const int tiles_n = (a.N + 63) / 64;
+  const int bm = (blockIdx.x / tiles_n) * 64, bn = (blockIdx.x % tiles_n) * 64;
+  const int t = threadIdx.x;
+  const int mr = t >> 2, c4 = (t & 3) * 4;
+  float acc[4][4] = {};
+  const T* A = static_cast<const T*>(a.A);
+  const T* W = static_cast<const T*>(a.W);
+  for (int k0 = 0; k0 < a.K; k0 += 16) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int idx = t + 256 * v, r = idx >> 4, c = idx & 15;
+      int gm = bm + r;
+      gm = gm < a.M ? gm : a.M - 1;
+      int gn = bn + r;
+      gn = gn < a.N ? gn : a.N - 1;
+      const bool kin = k0 + c < a.K;
+      sA[r][c] = kin ? to_f32(A[static_cast<long long>(gm) * a.lda + k0 + c]) : 0.f;
+      sB[r][c] = kin ? to_f32(W[static_cast<long long>(gn) * a.ldw + k0 + c]) : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < 16; ++kk) {
+      const float x = sA[mr][kk];
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[j][r] = fmaf(x, sB[16 * j + c4 + r][kk], acc[j][r]);
+    }
+    __syncthreads();
+  }
+  SiteMax sm;
+  const int m = bm + mr;
+#pragma unroll
+  for (int j = 0; j < 4; j += 2) epi_pair<T>(a, m, bn + 16 * j + c4, acc[j], acc[j + 1], sm);
+  site_flush(a, sm);
+}
+
+static bool g_force_simple = false;
+void gemm_force_simple(bool on) { g_force_simple = on; }
+
+void launch_gemm(const GemmArgs& a, hipStream_t s) {
+  if (a.dtype == kF32 || g_force_simple) {
+    const dim3 grid(((a.M + 63) / 64) * ((a.N + 63) / 64));
+    if (a.dtype == kF32) hipLaunchKernelGGL(k_gemm_simple<float>, grid, dim3(256), 0, s, a);
+    else if (a.dtype == kBF16) hipLaunchKernelGGL(k_gemm_simple<bf16_t>, grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(k_gemm_simple<f16_t>, grid, dim3(256), 0, s, a);
+    return;
+  }
+  const dim3 grid(((a.M + kBM - 1) / kBM) * ((a.N + kBN - 1) / kBN));
+  if (a.dtype == kBF16) hipLaunchKernelGGL(k_gemm_mfma<bf16_t>, grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(k_gemm_mfma<f16_t>, grid, dim3(256), 0, s, a);
+}
+
+}  // namespace gm

@@ -1,0 +1,724 @@
+// gm_runtime.cpp -- host runtime behind include/gm.h: configuration checks,
+// weight copy and repack, workspace and device state, the single-stream
+// enqueue of one forward, hipGraph capture with an exec cache, and the
+// synchronising readers (decisions, trap word, deferred effects).
+#include <hip/hip_runtime.h>
+
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "gm.h"
+#include "gm_device.h"
+#include "gm_kernels.h"
+
+namespace gm {
+void gemm_force_simple(bool on);
+void attention_force_rows(bool on);
+}
+
+using namespace gm;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int hip_fail(hipError_t e, const char* what) {
+  g_last_error = std::string(what) + ": " + hipGetErrorString(e);
+  return GM_E_HIP;
+}
+int inval(const char* what) {
+  g_last_error = what;
+  return GM_E_INVAL;
+}
+
+#define HIP_TRY(call)                                   \
+  do {                                                  \
+    hipError_t e_ = (call);                             \
+    if (e_ != hipSuccess) return hip_fail(e_, #call);   \
+  } while (0)
+
+struct LayerBufs {
+  void *ln1_g = nullptr, *ln1_b = nullptr, *wqkv = nullptr, *bqkv = nullptr;
+  void *wo = nullptr, *bo = nullptr, *ln2_g = nullptr, *ln2_b = nullptr;
+  void *w1 = nullptr, *b1 = nullptr, *w2 = nullptr, *b2 = nullptr;
+};
+
+struct GraphEntry {
+  int B, S;
+  const void *ids, *mask;
+  void* logits;
+  hipGraphExec_t exec;
+  uint64_t last_use;
+};
+
+constexpr int kFifoCap = 4096;
+constexpr int kMaxGraphs = 8;
+
+}  // namespace
+
+struct gm_model {
+  gm_config cfg;
+  int device = 0;
+  int dtype = 0;
+  size_t esz = 0;
+  std::vector<void*> allocs;
+  void *tok_emb = nullptr, *pos_emb = nullptr, *emb_ln_g = nullptr, *emb_ln_b = nullptr;
+  void *lnf_g = nullptr, *lnf_b = nullptr, *head = nullptr;
+  std::vector<LayerBufs> layers;
+  void *h = nullptr, *a = nullptr, *qkv = nullptr, *ctx = nullptr, *f = nullptr, *tmp = nullptr;
+  int32_t* state = nullptr;
+  int n_state = 0;
+  float *rope_cos = nullptr, *rope_sin = nullptr;
+  void* fifo = nullptr;
+  hipStream_t cap_stream = nullptr;
+  std::vector<GraphEntry> graphs;
+  gm_stats stats;
+  bool graph_mode = true;
+  bool debug_sync = false;
+  uint64_t tick = 0;
+
+  int alloc(void** p, size_t bytes) {
+    *p = nullptr;
+    if (bytes == 0) return GM_OK;
+    hipError_t e = hipMalloc(p, bytes);
+    if (e != hipSuccess) {
+      g_last_error = std::string("hipMalloc: ") + hipGetErrorString(e);
+      *p = nullptr;
+      return GM_E_NOMEM;
+    }
+    allocs.push_back(*p);
+    return GM_OK;
+  }
+};
+
+namespace {
+
+int n_sites(const gm_config& c) { return c.fp16_clamp ? 2 * c.n_layers : 0; }
+
+int validate(const gm_config* c) {
+  if (!c) return inval("cfg is NULL");
+  if (c->abi_version != GM_ABI_VERSION) return inval("abi_version mismatch");
+  if (c->n_layers < 1 || c->n_layers > GM_MAX_LAYERS) return inval("n_layers out of [1, 64]");
+  if (c->d_model <= 0 || c->n_heads <= 0 || c->d_model % c->n_heads)
+    return inval("d_model must be a positive multiple of n_heads");
+  const int hd = c->d_model / c->n_heads;
+  if (hd != 32 && hd != 64 && hd != 128) return inval("head_dim must be 32, 64 or 128");
+  if (c->d_ff <= 0 || c->vocab <= 0) return inval("d_ff and vocab must be positive");
+  if (c->act_dtype < GM_DTYPE_F32 || c->act_dtype > GM_DTYPE_F16) return inval("bad act_dtype");
+  if (c->act_dtype == GM_DTYPE_F32) {
+    if (c->d_model % 64 || c->d_ff % 64) return inval("d_model and d_ff must be multiples of 64");
+  } else {
+    if (c->d_model % 64 || c->d_ff % 64) return inval("d_model and d_ff must be multiples of 64");
+  }
+  if (c->max_batch < 1 || c->max_batch > 1024) return inval("max_batch out of [1, 1024]");
+  if (c->max_seq < 1) return inval("max_seq must be positive");
+  if (static_cast<long long>(c->max_batch) * c->max_seq >= (1ll << 24))
+    return inval("max_batch * max_seq must be < 2^24");
+  if (c->norm != GM_NORM_LAYER && c->norm != GM_NORM_RMS) return inval("bad norm");
+  if (c->norm_place != GM_NORM_PRE && c->norm_place != GM_NORM_POST) return inval("bad norm_place");
+  if (c->ffn < GM_FFN_GELU || c->ffn > GM_FFN_SWIGLU) return inval("bad ffn");
+  if (c->pos < GM_POS_NONE || c->pos > GM_POS_ROTARY) return inval("bad pos");
+  if (!(c->norm_eps > 0.f)) return inval("norm_eps must be positive");
+  if (c->pos == GM_POS_ROTARY) {
+    if (c->rope_capacity < 1 || c->rope_init_len < 0 || c->rope_init_len > c->rope_capacity)
+      return inval("need 0 <= rope_init_len <= rope_capacity, capacity >= 1");
+    if (!(c->rope_base > 1.f)) return inval("rope_base must be > 1");
+  }
+  if (c->fp16_clamp) {
+    if (c->act_dtype != GM_DTYPE_F16) return inval("fp16_clamp needs act_dtype f16");
+    if (c->norm_place != GM_NORM_PRE) return inval("fp16_clamp needs pre-norm");
+    if (!(c->clamp_margin >= 0.f) || c->clamp_margin >= 65504.f) return inval("bad clamp_margin");
+  }
+  return GM_OK;
+}
+
+// Copy a caller tensor into library memory (optionally permuting rows).
+int copy_in(gm_model* m, void** dst, const void* src, size_t rows, size_t cols,
+            const std::vector<int32_t>* perm, const char* name) {
+  if (!src) {
+    g_last_error = std::string("weight ") + name + " is NULL";
+    return GM_E_INVAL;
+  }
+  const size_t row_bytes = cols * m->esz;
+  int rc = m->alloc(dst, rows * row_bytes);
+  if (rc) return rc;
+  if (!perm) {
+    HIP_TRY(hipMemcpy(*dst, src, rows * row_bytes, hipMemcpyDeviceToDevice));
+    return GM_OK;
+  }
+  if (row_bytes % 16 == 0) {
+    int32_t* dmap = nullptr;
+    HIP_TRY(hipMalloc(&dmap, rows * sizeof(int32_t)));
+    hipError_t e = hipMemcpy(dmap, perm->data(), rows * sizeof(int32_t), hipMemcpyHostToDevice);
+    if (e == hipSuccess) {
+      launch_gather_rows(*dst, src, dmap, static_cast<int>(rows), static_cast<int>(row_bytes), nullptr);
+      e = hipGetLastError();
+    }
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    hipFree(dmap);
+    if (e != hipSuccess) return hip_fail(e, "repack");
+    return GM_OK;
+  }
+  // small tensors (bias vectors): permute on the host
+  std::vector<unsigned char> hs(rows * row_bytes), hd(rows * row_bytes);
+  HIP_TRY(hipMemcpy(hs.data(), src, hs.size(), hipMemcpyDeviceToHost));
+  for (size_t r = 0; r < rows; ++r)
+    memcpy(&hd[r * row_bytes], &hs[static_cast<size_t>((*perm)[r]) * row_bytes], row_bytes);
+  HIP_TRY(hipMemcpy(*dst, hd.data(), hd.size(), hipMemcpyHostToDevice));
+  return GM_OK;
+}
+
+// Packed order of gated FFN rows: 16 gate rows, then the 16 matching up rows.
+std::vector<int32_t> gated_perm(int ff) {
+  std::vector<int32_t> p(2 * ff);
+  for (int n = 0; n < 2 * ff; ++n) {
+    const int grp = n / 32, q = n % 32;
+    p[n] = q < 16 ? grp * 16 + q : ff + grp * 16 + (q - 16);
+  }
+  return p;
+}
+
+// Packed order of q/k rows for rotary: inside each head, 16 rows i, then the
+// 16 rows i + hd/2 they rotate with.  v rows keep their order.
+std::vector<int32_t> rope_perm(int d, int hd) {
+  std::vector<int32_t> p(3 * d);
+  for (int n = 0; n < 3 * d; ++n) {
+    if (n >= 2 * d) {
+      p[n] = n;
+      continue;
+    }
+    const int region = n / d, nr = n % d, h = nr / hd, w = nr % hd;
+    const int i = (w / 32) * 16 + (w % 16);
+    const bool second = (w % 32) >= 16;
+    p[n] = region * d + h * hd + (second ? i + hd / 2 : i);
+  }
+  return p;
+}
+
+// Per-launch event timing for gm_profile_forward: an event is recorded on
+// the launch stream after every kernel, with the kernel kind, its layer and
+// its algorithmic work.
+struct Prof {
+  hipStream_t s;
+  std::vector<hipEvent_t> ev;
+  std::vector<gm_kernel_time> rec;
+  bool ok = true;
+  void start() { mark_event(); }
+  void mark_event() {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) {
+      ok = false;
+      return;
+    }
+    hipEventRecord(e, s);
+    ev.push_back(e);
+  }
+  void mark(int kind, int layer, double flops, double bytes) {
+    gm_kernel_time r;
+    r.kind = kind;
+    r.layer = layer;
+    r.ms = 0.f;
+    r.flops = flops;
+    r.bytes = bytes;
+    rec.push_back(r);
+    mark_event();
+  }
+};
+
+void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
+             void* logits, hipStream_t s, Prof* prof = nullptr) {
+  const gm_config& c = m->cfg;
+  const int T = B * S, d = c.d_model, hd = d / c.n_heads, ff = c.d_ff;
+  const int ns = n_sites(c);
+  const float thr = 65504.f - c.clamp_margin;
+  const bool pre = c.norm_place == GM_NORM_PRE;
+  const int normk = c.norm == GM_NORM_RMS ? 1 : 0;
+
+  const double es = static_cast<double>(m->esz);
+  int cur_layer = -1;
+  auto P = [&](int kind, int layer, double flops, double bytes) {
+    if (prof) prof->mark(kind, layer, flops, bytes);
+  };
+  if (prof) prof->start();
+  launch_prologue(ids, mask, B, S, c.vocab, c.pos == GM_POS_ROTARY, c.rope_capacity, ns,
+                  m->state, s);
+  P(GM_K_PROLOGUE, -1, 0.0, 8.0 * T);
+  if (c.pos == GM_POS_ROTARY) {
+    launch_rope_fill(m->rope_cos, m->rope_sin, hd, c.rope_base, m->state, s);
+    P(GM_K_ROPE, -1, 0.0, 0.0);
+  }
+
+  RowArgs r{};
+  r.dtype = m->dtype;
+  r.rows = T;
+  r.d = d;
+  r.eps = c.norm_eps;
+  r.state = m->state;
+  r.clamp_thr = thr;
+  // embedding (+ embedding norm)
+  r.ids = ids;
+  r.tok_emb = m->tok_emb;
+  r.pos_emb = c.pos == GM_POS_LEARNED ? m->pos_emb : nullptr;
+  r.seq = S;
+  r.vocab = c.vocab;
+  r.x = m->h;
+  r.norm = c.emb_norm ? normk : -1;
+  r.g = m->emb_ln_g;
+  r.b = m->emb_ln_b;
+  r.out = m->h;
+  r.clamp_site = -1;
+  launch_rownorm(r, s);
+  P(GM_K_EMBED, -1, 0.0, static_cast<double>(T) * d * es * (c.pos == GM_POS_LEARNED ? 3 : 2));
+  r.ids = nullptr;
+
+  auto norm_rows = [&](void* x, void* out, const void* g, const void* b, int site) {
+    RowArgs q = r;
+    q.x = x;
+    q.out = out;
+    q.norm = normk;
+    q.g = g;
+    q.b = b;
+    q.clamp_site = site;
+    launch_rownorm(q, s);
+    P(GM_K_NORM, cur_layer, 0.0, 2.0 * T * d * es);
+  };
+
+  GemmArgs ga{};
+  ga.dtype = m->dtype;
+  ga.M = T;
+  ga.state = m->state;
+  ga.site = -1;
+  ga.seq = S;
+  ga.head_dim = hd;
+  ga.d_model = d;
+  ga.rope_cos = m->rope_cos;
+  ga.rope_sin = m->rope_sin;
+  ga.rope_rows = c.rope_capacity > 0 ? c.rope_capacity : 1;
+  auto gemm = [&](int kind, const void* A, int K, const void* W, int N, int epi, const void* bias,
+                  void* out, int ldo, const void* resid, int site) {
+    GemmArgs q = ga;
+    q.A = A;
+    q.lda = K;
+    q.K = K;
+    q.W = W;
+    q.ldw = K;
+    q.N = N;
+    q.epi = epi;
+    q.bias = bias;
+    q.out = out;
+    q.ldo = ldo;
+    q.resid = resid;
+    q.ldr = ldo;
+    q.site = site;
+    launch_gemm(q, s);
+    const int nout = (epi == kEpiGatedGelu || epi == kEpiGatedSilu) ? N / 2 : N;
+    P(kind, cur_layer, 2.0 * T * static_cast<double>(N) * K,
+      es * (static_cast<double>(T) * K + static_cast<double>(N) * K +
+            static_cast<double>(T) * nout * (resid ? 2 : 1)));
+  };
+
+  AttnArgs at{};
+  at.dtype = m->dtype;
+  at.B = B;
+  at.S = S;
+  at.H = c.n_heads;
+  at.hd = hd;
+  at.d = d;
+  at.qkv = m->qkv;
+  at.ctx = m->ctx;
+  at.mask = mask;
+  at.state = m->state;
+  at.causal = c.causal;
+  at.scale = 1.0f / sqrtf(static_cast<float>(hd));
+
+  const int up_epi = c.ffn == GM_FFN_GELU ? kEpiGelu
+                     : c.ffn == GM_FFN_GEGLU ? kEpiGatedGelu : kEpiGatedSilu;
+  const int up_n = c.ffn == GM_FFN_GELU ? ff : 2 * ff;
+  const int qkv_epi = c.pos == GM_POS_ROTARY ? kEpiRope : kEpiStore;
+  const double pairs = c.causal ? 0.5 * S * (S + 1.0) : static_cast<double>(S) * S;
+  const double attn_flops = 4.0 * hd * pairs * B * c.n_heads;
+  const double attn_bytes = es * (static_cast<double>(T) * 3 * d + static_cast<double>(T) * d);
+  auto attention = [&]() {
+    launch_attention(at, s);
+    P(GM_K_ATTENTION, cur_layer, attn_flops, attn_bytes);
+  };
+  int prev_site = -1;
+  for (int l = 0; l < c.n_layers; ++l) {
+    cur_layer = l;
+    const LayerBufs& L = m->layers[l];
+    const int s0 = ns ? 2 * l : -1, s1 = ns ? 2 * l + 1 : -1;
+    if (pre) {
+      norm_rows(m->h, m->a, L.ln1_g, L.ln1_b, prev_site);
+      gemm(GM_K_GEMM_QKV, m->a, d, L.wqkv, 3 * d, qkv_epi, L.bqkv, m->qkv, 3 * d, nullptr, -1);
+      attention();
+      gemm(GM_K_GEMM_O, m->ctx, d, L.wo, d, kEpiResid, L.bo, m->h, d, m->h, s0);
+      norm_rows(m->h, m->a, L.ln2_g, L.ln2_b, s0);
+      gemm(GM_K_GEMM_UP, m->a, d, L.w1, up_n, up_epi, L.b1, m->f, ff, nullptr, -1);
+      gemm(GM_K_GEMM_DOWN, m->f, ff, L.w2, d, kEpiResid, L.b2, m->h, d, m->h, s1);
+      prev_site = s1;
+    } else {
+      gemm(GM_K_GEMM_QKV, m->h, d, L.wqkv, 3 * d, qkv_epi, L.bqkv, m->qkv, 3 * d, nullptr, -1);
+      attention();
+      gemm(GM_K_GEMM_O, m->ctx, d, L.wo, d, kEpiResid, L.bo, m->tmp, d, m->h, -1);
+      norm_rows(m->tmp, m->h, L.ln1_g, L.ln1_b, -1);
+      gemm(GM_K_GEMM_UP, m->h, d, L.w1, up_n, up_epi, L.b1, m->f, ff, nullptr, -1);
+      gemm(GM_K_GEMM_DOWN, m->f, ff, L.w2, d, kEpiResid, L.b2, m->tmp, d, m->h, -1);
+      norm_rows(m->tmp, m->h, L.ln2_g, L.ln2_b, -1);
+    }
+  }
+  cur_layer = -1;
+  const void* z = m->h;
+  if (pre) {
+    norm_rows(m->h, m->a, m->lnf_g, m->lnf_b, prev_site);
+    z = m->a;
+  }
+  gemm(GM_K_GEMM_HEAD, z, d, m->head, c.vocab, kEpiStore, nullptr, logits, c.vocab, nullptr, -1);
+  launch_emit_effects(m->state, m->fifo, kFifoCap, ns, s);
+  P(GM_K_EFFECTS, -1, 0.0, 0.0);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* gm_strerror(int code) {
+  switch (code) {
+    case GM_OK: return "ok";
+    case GM_E_INVAL: return "invalid argument";
+    case GM_E_NOMEM: return "out of device memory";
+    case GM_E_HIP: return "HIP runtime error";
+    case GM_E_CAPTURE: return "graph capture failed";
+    default: return "unknown error";
+  }
+}
+
+const char* gm_last_error(void) { return g_last_error.c_str(); }
+
+void gm_model_destroy(gm_model* m) {
+  if (!m) return;
+  hipDeviceSynchronize();
+  for (auto& g : m->graphs) hipGraphExecDestroy(g.exec);
+  if (m->cap_stream) hipStreamDestroy(m->cap_stream);
+  for (void* p : m->allocs) hipFree(p);
+  delete m;
+}
+
+int gm_model_create(const gm_config* cfg, const gm_weights* w, gm_model** out) {
+  if (!out) return inval("out is NULL");
+  *out = nullptr;
+  int rc = validate(cfg);
+  if (rc) return rc;
+  if (!w || !w->layers) return inval("weights or weights->layers is NULL");
+  const gm_config& c = *cfg;
+  const bool ln = c.norm == GM_NORM_LAYER;
+  const bool pre = c.norm_place == GM_NORM_PRE;
+  // unused pointers must be NULL, used ones non-NULL
+  auto want = [&](const void* p, bool used, const char* name) -> int {
+    if (used && !p) return inval((std::string("missing weight ") + name).c_str());
+    if (!used && p) return inval((std::string("unexpected weight ") + name).c_str());
+    return GM_OK;
+  };
+  if ((rc = want(w->tok_emb, true, "tok_emb")) || (rc = want(w->pos_emb, c.pos == GM_POS_LEARNED, "pos_emb")) ||
+      (rc = want(w->emb_ln_g, c.emb_norm, "emb_ln_g")) || (rc = want(w->emb_ln_b, c.emb_norm && ln, "emb_ln_b")) ||
+      (rc = want(w->lnf_g, pre, "lnf_g")) || (rc = want(w->lnf_b, pre && ln, "lnf_b")) ||
+      (rc = want(w->lm_head, !c.tied_head, "lm_head")))
+    return rc;
+  for (int l = 0; l < c.n_layers; ++l) {
+    const gm_layer_weights& L = w->layers[l];
+    if ((rc = want(L.ln1_g, true, "ln1_g")) || (rc = want(L.ln1_b, ln, "ln1_b")) ||
+        (rc = want(L.ln2_g, true, "ln2_g")) || (rc = want(L.ln2_b, ln, "ln2_b")) ||
+        (rc = want(L.wqkv, true, "wqkv")) || (rc = want(L.wo, true, "wo")) ||
+        (rc = want(L.w1, true, "w1")) || (rc = want(L.w2, true, "w2")) ||
+        (rc = want(L.bqkv, c.has_bias, "bqkv")) || (rc = want(L.bo, c.has_bias, "bo")) ||
+        (rc = want(L.b1, c.has_bias, "b1")) || (rc = want(L.b2, c.has_bias, "b2")))
+      return rc;
+  }
+
+  gm_model* m = new gm_model();
+  m->cfg = c;
+  m->dtype = c.act_dtype;
+  m->esz = c.act_dtype == GM_DTYPE_F32 ? 4 : 2;
+  memset(&m->stats, 0, sizeof(m->stats));
+  m->debug_sync = getenv("GM_DEBUG_SYNC") && atoi(getenv("GM_DEBUG_SYNC"));
+  gemm_force_simple(getenv("GM_SIMPLE_GEMM") && atoi(getenv("GM_SIMPLE_GEMM")));
+  attention_force_rows(getenv("GM_SIMPLE_ATTN") && atoi(getenv("GM_SIMPLE_ATTN")));
+  auto fail = [&](int code) {
+    gm_model_destroy(m);
+    return code;
+  };
+  hipError_t e = hipGetDevice(&m->device);
+  if (e != hipSuccess) return fail(hip_fail(e, "hipGetDevice"));
+
+  const int d = c.d_model, hd = d / c.n_heads, ff = c.d_ff, V = c.vocab;
+  const bool gated = c.ffn != GM_FFN_GELU;
+  const std::vector<int32_t> gp = gated ? gated_perm(ff) : std::vector<int32_t>();
+  const std::vector<int32_t> rp = c.pos == GM_POS_ROTARY ? rope_perm(d, hd) : std::vector<int32_t>();
+  const std::vector<int32_t>* gpp = gated ? &gp : nullptr;
+  const std::vector<int32_t>* rpp = c.pos == GM_POS_ROTARY ? &rp : nullptr;
+
+  if ((rc = copy_in(m, &m->tok_emb, w->tok_emb, V, d, nullptr, "tok_emb"))) return fail(rc);
+  if (c.pos == GM_POS_LEARNED && (rc = copy_in(m, &m->pos_emb, w->pos_emb, c.max_seq, d, nullptr, "pos_emb")))
+    return fail(rc);
+  if (c.emb_norm) {
+    if ((rc = copy_in(m, &m->emb_ln_g, w->emb_ln_g, 1, d, nullptr, "emb_ln_g"))) return fail(rc);
+    if (ln && (rc = copy_in(m, &m->emb_ln_b, w->emb_ln_b, 1, d, nullptr, "emb_ln_b"))) return fail(rc);
+  }
+  if (pre) {
+    if ((rc = copy_in(m, &m->lnf_g, w->lnf_g, 1, d, nullptr, "lnf_g"))) return fail(rc);
+    if (ln && (rc = copy_in(m, &m->lnf_b, w->lnf_b, 1, d, nullptr, "lnf_b"))) return fail(rc);
+  }
+  if (c.tied_head) m->head = m->tok_emb;
+  else if ((rc = copy_in(m, &m->head, w->lm_head, V, d, nullptr, "lm_head"))) return fail(rc);
+
+  m->layers.resize(c.n_layers);
+  for (int l = 0; l < c.n_layers; ++l) {
+    const gm_layer_weights& L = w->layers[l];
+    LayerBufs& B = m->layers[l];
+    const int f1 = gated ? 2 * ff : ff;
+    if ((rc = copy_in(m, &B.ln1_g, L.ln1_g, 1, d, nullptr, "ln1_g")) ||
+        (ln && (rc = copy_in(m, &B.ln1_b, L.ln1_b, 1, d, nullptr, "ln1_b"))) ||
+        (rc = copy_in(m, &B.ln2_g, L.ln2_g, 1, d, nullptr, "ln2_g")) ||
+        (ln && (rc = copy_in(m, &B.ln2_b, L.ln2_b, 1, d, nullptr, "ln2_b"))) ||
+        (rc = copy_in(m, &B.wqkv, L.wqkv, 3 * d, d, rpp, "wqkv")) ||
+        (rc = copy_in(m, &B.wo, L.wo, d, d, nullptr, "wo")) ||
+        (rc = copy_in(m, &B.w1, L.w1, f1, d, gpp, "w1")) ||
+        (rc = copy_in(m, &B.w2, L.w2, d, ff, nullptr, "w2")))
+      return fail(rc);
+    if (c.has_bias) {
+      if ((rc = copy_in(m, &B.bqkv, L.bqkv, 3 * d, 1, rpp, "bqkv")) ||
+          (rc = copy_in(m, &B.bo, L.bo, d, 1, nullptr, "bo")) ||
+          (rc = copy_in(m, &B.b1, L.b1, f1, 1, gpp, "b1")) ||
+          (rc = copy_in(m, &B.b2, L.b2, d, 1, nullptr, "b2")))
+        return fail(rc);
+    }
+  }
+
+  // workspace
+  const size_t T = static_cast<size_t>(c.max_batch) * c.max_seq;
+  const size_t es = m->esz;
+  if ((rc = m->alloc(&m->h, T * d * es)) || (rc = m->alloc(&m->a, T * d * es)) ||
+      (rc = m->alloc(&m->qkv, T * 3 * d * es)) || (rc = m->alloc(&m->ctx, T * d * es)) ||
+      (rc = m->alloc(&m->f, T * ff * es)) ||
+      (!pre && (rc = m->alloc(&m->tmp, T * d * es))))
+    return fail(rc);
+  // device state
+  m->n_state = kKvLenBase + c.max_batch;
+  void* p = nullptr;
+  if ((rc = m->alloc(&p, m->n_state * sizeof(int32_t)))) return fail(rc);
+  m->state = static_cast<int32_t*>(p);
+  if ((rc = m->alloc(&m->fifo, kFifoCap * sizeof(EffectRec)))) return fail(rc);
+  std::vector<int32_t> st(m->n_state, 0);
+  st[kTrapFwd] = static_cast<int32_t>(kTrapNone);
+  if (c.pos == GM_POS_ROTARY) {
+    const size_t tb = static_cast<size_t>(c.rope_capacity) * (hd / 2) * sizeof(float);
+    if ((rc = m->alloc(&p, tb))) return fail(rc);
+    m->rope_cos = static_cast<float*>(p);
+    if ((rc = m->alloc(&p, tb))) return fail(rc);
+    m->rope_sin = static_cast<float*>(p);
+    e = hipMemset(m->rope_cos, 0, tb);
+    if (e == hipSuccess) e = hipMemset(m->rope_sin, 0, tb);
+    if (e != hipSuccess) return fail(hip_fail(e, "hipMemset"));
+    st[kRegrowFrom] = 0;
+    st[kRegrowTo] = c.rope_init_len;
+    st[kCachedLen] = c.rope_init_len;
+  }
+  e = hipMemcpy(m->state, st.data(), st.size() * sizeof(int32_t), hipMemcpyHostToDevice);
+  if (e != hipSuccess) return fail(hip_fail(e, "state init"));
+  if (c.pos == GM_POS_ROTARY) {
+    // rows [0, rope_init_len) with the same kernel that grows the table
+    launch_rope_fill(m->rope_cos, m->rope_sin, hd, c.rope_base, m->state, nullptr);
+    e = hipGetLastError();
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    if (e != hipSuccess) return fail(hip_fail(e, "rope init"));
+  }
+  e = hipStreamCreateWithFlags(&m->cap_stream, hipStreamNonBlocking);
+  if (e != hipSuccess) return fail(hip_fail(e, "hipStreamCreate"));
+  e = hipDeviceSynchronize();
+  if (e != hipSuccess) return fail(hip_fail(e, "create"));
+  *out = m;
+  return GM_OK;
+}
+
+int gm_set_graph_mode(gm_model* m, int32_t enabled) {
+  if (!m) return inval("model is NULL");
+  m->graph_mode = enabled != 0;
+  return GM_OK;
+}
+
+int gm_forward_ex(gm_model* m, int32_t B, int32_t S, const int32_t* ids, const int32_t* mask,
+                  void* logits, hipStream_t stream) {
+  if (!m) return inval("model is NULL");
+  if (!ids || !mask || !logits) return inval("ids, mask and logits must be non-NULL");
+  if (B < 1 || B > m->cfg.max_batch || S < 1 || S > m->cfg.max_seq)
+    return inval("B or S out of range");
+  m->stats.forwards++;
+  if (!m->graph_mode) {
+    enqueue(m, B, S, ids, mask, logits, stream);
+    HIP_TRY(hipGetLastError());
+    m->stats.eager_forwards++;
+    if (m->debug_sync) {
+      m->stats.host_syncs_in_forward++;
+      HIP_TRY(hipStreamSynchronize(stream));
+    }
+    return GM_OK;
+  }
+  GraphEntry* ge = nullptr;
+  for (auto& g : m->graphs)
+    if (g.B == B && g.S == S && g.ids == ids && g.mask == mask && g.logits == logits) ge = &g;
+  if (!ge) {
+    hipGraph_t graph = nullptr;
+    HIP_TRY(hipStreamBeginCapture(m->cap_stream, hipStreamCaptureModeThreadLocal));
+    enqueue(m, B, S, ids, mask, logits, m->cap_stream);
+    hipError_t e = hipStreamEndCapture(m->cap_stream, &graph);
+    if (e != hipSuccess || !graph) {
+      g_last_error = std::string("capture: ") + hipGetErrorString(e);
+      hipGetLastError();
+      return GM_E_CAPTURE;
+    }
+    size_t nodes = 0;
+    hipGraphGetNodes(graph, nullptr, &nodes);
+    hipGraphExec_t exec = nullptr;
+    e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+    hipGraphDestroy(graph);
+    if (e != hipSuccess) {
+      g_last_error = std::string("instantiate: ") + hipGetErrorString(e);
+      return GM_E_CAPTURE;
+    }
+    if (static_cast<int>(m->graphs.size()) >= kMaxGraphs) {
+      size_t victim = 0;
+      for (size_t i = 1; i < m->graphs.size(); ++i)
+        if (m->graphs[i].last_use < m->graphs[victim].last_use) victim = i;
+      hipGraphExecDestroy(m->graphs[victim].exec);
+      m->graphs.erase(m->graphs.begin() + victim);
+    }
+    m->graphs.push_back(GraphEntry{B, S, ids, mask, logits, exec, 0});
+    ge = &m->graphs.back();
+    m->stats.captures++;
+    m->stats.kernels_per_forward = nodes;
+  }
+  ge->last_use = ++m->tick;
+  HIP_TRY(hipGraphLaunch(ge->exec, stream));
+  m->stats.graph_launches++;
+  if (m->debug_sync) {
+    m->stats.host_syncs_in_forward++;
+    HIP_TRY(hipStreamSynchronize(stream));
+  }
+  return GM_OK;
+}
+
+int gm_profile_forward(gm_model* m, int32_t B, int32_t S, const int32_t* ids,
+                       const int32_t* mask, void* logits, hipStream_t stream,
+                       gm_kernel_time* out, int32_t cap, int32_t* n_out) {
+  if (!m || !out || !n_out) return inval("NULL argument");
+  if (!ids || !mask || !logits) return inval("ids, mask and logits must be non-NULL");
+  if (B < 1 || B > m->cfg.max_batch || S < 1 || S > m->cfg.max_seq)
+    return inval("B or S out of range");
+  Prof prof;
+  prof.s = stream;
+  enqueue(m, B, S, ids, mask, logits, stream, &prof);
+  hipError_t e = hipGetLastError();
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  int rc = GM_OK;
+  if (e != hipSuccess) rc = hip_fail(e, "profile");
+  else if (!prof.ok || prof.ev.size() != prof.rec.size() + 1) rc = inval("event creation failed");
+  const int n = static_cast<int>(prof.rec.size());
+  *n_out = n;
+  for (int i = 0; rc == GM_OK && i < n && i < cap; ++i) {
+    float ms = 0.f;
+    hipEventElapsedTime(&ms, prof.ev[i], prof.ev[i + 1]);
+    out[i] = prof.rec[i];
+    out[i].ms = ms;
+  }
+  for (hipEvent_t ev : prof.ev) hipEventDestroy(ev);
+  return rc;
+}
+
+int gm_forward(gm_model* m, const int32_t* ids, const int32_t* mask, void* logits,
+               hipStream_t stream) {
+  if (!m) return inval("model is NULL");
+  return gm_forward_ex(m, m->cfg.max_batch, m->cfg.max_seq, ids, mask, logits, stream);
+}
+
+int gm_read_decisions(gm_model* m, gm_decisions* out, hipStream_t stream) {
+  if (!m || !out) return inval("model or out is NULL");
+  HIP_TRY(hipStreamSynchronize(stream));
+  std::vector<int32_t> st(m->n_state);
+  HIP_TRY(hipMemcpy(st.data(), m->state, st.size() * sizeof(int32_t), hipMemcpyDeviceToHost));
+  memset(out, 0, sizeof(*out));
+  out->pad_any = st[kPadAny];
+  out->regrow = st[kRegrow];
+  out->need = st[kNeed];
+  out->cached_len = st[kCachedLen];
+  out->n_clamp_sites = n_sites(m->cfg);
+  for (int i = 0; i < out->n_clamp_sites; ++i) {
+    out->clamp[i] = st[kClampBase + i];
+    uint32_t u = static_cast<uint32_t>(st[kAbsmaxBase + i]);
+    float f;
+    memcpy(&f, &u, 4);
+    out->clamp_absmax[i] = f;
+    out->clamp_nan[i] = st[kNanBase + i];
+  }
+  out->forward_index = st[kFwdIndex];
+  return GM_OK;
+}
+
+const int32_t* gm_decisions_device_ptr(const gm_model* m) { return m ? m->state : nullptr; }
+
+int gm_check_error(gm_model* m, int32_t* code, int32_t* index) {
+  if (!m || !code || !index) return inval("NULL argument");
+  HIP_TRY(hipDeviceSynchronize());
+  int32_t w = 0;
+  HIP_TRY(hipMemcpy(&w, m->state + kTrapSticky, sizeof(w), hipMemcpyDeviceToHost));
+  const uint32_t u = static_cast<uint32_t>(w);
+  *code = w ? static_cast<int32_t>(u >> 24) : GM_TRAP_NONE;
+  *index = w ? static_cast<int32_t>(u & 0xFFFFFFu) : 0;
+  const int32_t zero = 0;
+  HIP_TRY(hipMemcpy(m->state + kTrapSticky, &zero, sizeof(zero), hipMemcpyHostToDevice));
+  return GM_OK;
+}
+
+int gm_flush_effects(gm_model* m, gm_effect_cb cb, void* user, int32_t* n_dropped) {
+  if (!m) return inval("model is NULL");
+  HIP_TRY(hipDeviceSynchronize());
+  int32_t cd[2];
+  HIP_TRY(hipMemcpy(cd, m->state + kFifoCount, sizeof(cd), hipMemcpyDeviceToHost));
+  const int n = cd[0] < kFifoCap ? cd[0] : kFifoCap;
+  std::vector<EffectRec> recs(n);
+  if (n) HIP_TRY(hipMemcpy(recs.data(), m->fifo, n * sizeof(EffectRec), hipMemcpyDeviceToHost));
+  const int32_t zero[2] = {0, 0};
+  HIP_TRY(hipMemcpy(m->state + kFifoCount, zero, sizeof(zero), hipMemcpyHostToDevice));
+  if (n_dropped) *n_dropped = cd[1];
+  if (cb)
+    for (const EffectRec& r : recs) {
+      gm_effect e{r.forward, r.kind, r.layer, r.site, r.value};
+      cb(&e, user);
+    }
+  return GM_OK;
+}
+
+int gm_debug_buffer(const gm_model* m, int32_t which, void** ptr, uint64_t* bytes) {
+  if (!m || !ptr || !bytes) return inval("NULL argument");
+  const gm_config& c = m->cfg;
+  const uint64_t T = static_cast<uint64_t>(c.max_batch) * c.max_seq;
+  const uint64_t d = c.d_model;
+  switch (which) {
+    case 0: *ptr = m->h; *bytes = T * d * m->esz; break;
+    case 1: *ptr = m->a; *bytes = T * d * m->esz; break;
+    case 2: *ptr = m->qkv; *bytes = T * 3 * d * m->esz; break;
+    case 3: *ptr = m->ctx; *bytes = T * d * m->esz; break;
+    case 4: *ptr = m->f; *bytes = T * c.d_ff * m->esz; break;
+    default: return inval("which out of [0, 4]");
+  }
+  return GM_OK;
+}
+
+int gm_get_stats(const gm_model* m, gm_stats* out) {
+  if (!m || !out) return inval("NULL argument");
+  *out = m->stats;
+  return GM_OK;
+}
+
+}  // extern "C"
