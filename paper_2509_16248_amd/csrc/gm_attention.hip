@@ -157,8 +157,8 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
       int key = kb + r;
       key = key < S ? key : S - 1;
       const T* kp = base + static_cast<long long>(key) * ld + d + h * HD + c;
-      *reinterpret_cast<uint4*>(&sK[r * LDK + c]) = *reinterpret_cast<const uint4*>(kp);
-      const uint4 vv = *reinterpret_cast<const uint4*>(kp + d);
+      *reinterpret_cast<u32x4*>(&sK[r * LDK + c]) = *reinterpret_cast<const u32x4*>(kp);
+      const u32x4 vv = *reinterpret_cast<const u32x4*>(kp + d);
       const T* ve = reinterpret_cast<const T*>(&vv);
 #pragma unroll
       for (int e = 0; e < 8; ++e) sVt[(c + e) * LDV + r] = ve[e];
@@ -239,8 +239,8 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
       for (int c = 0; c < NCT; ++c) {
         const T* vr = &sVt[(16 * c + l16) * LDV + 32 * kc + 4 * g];
         T tmp[8];
-        *reinterpret_cast<uint2*>(&tmp[0]) = *reinterpret_cast<const uint2*>(vr);
-        *reinterpret_cast<uint2*>(&tmp[4]) = *reinterpret_cast<const uint2*>(vr + 16);
+        *reinterpret_cast<u32x2*>(&tmp[0]) = *reinterpret_cast<const u32x2*>(vr);
+        *reinterpret_cast<u32x2*>(&tmp[4]) = *reinterpret_cast<const u32x2*>(vr + 16);
         const vec vf = *reinterpret_cast<const vec*>(tmp);
 #pragma unroll
         for (int u = 0; u < 2; ++u) oacc[u][c] = MfmaA<T>::run(vf, pb[u], oacc[u][c]);
@@ -257,11 +257,11 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
     T* out = static_cast<T*>(a.ctx) + (static_cast<long long>(b) * S + qi) * d + h * HD;
 #pragma unroll
     for (int c = 0; c < NCT; ++c) {
-      uint2 r2;
+      u32x2 r2;
       T* e = reinterpret_cast<T*>(&r2);
 #pragma unroll
       for (int r = 0; r < 4; ++r) e[r] = from_f32<T>(oacc[u][c][r] * inv);
-      *reinterpret_cast<uint2*>(out + 16 * c + 4 * g) = r2;
+      *reinterpret_cast<u32x2*>(out + 16 * c + 4 * g) = r2;
     }
   }
 }

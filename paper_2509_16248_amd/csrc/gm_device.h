@@ -37,6 +37,14 @@ struct EffectRec {   // mirrors gm_effect
   float value;
 };
 
+// ------------------------------------------------------------ vector types
+// Native clang vector types for 8/16-byte memory accesses.  (HIP's uint4 /
+// float4 are structs with unions; arrays of them are not promoted to
+// registers and end up in scratch memory.)
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4v __attribute__((ext_vector_type(4)));
+
 // ------------------------------------------------------------ storage dtypes
 typedef uint16_t bf16_t;   // bfloat16 bit pattern
 typedef _Float16 f16_t;

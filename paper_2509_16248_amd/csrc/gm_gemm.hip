@@ -8,6 +8,8 @@
 // round once to the storage dtype.
 #include <math.h>
 
+#include <type_traits>
+
 #include "gm_device.h"
 #include "gm_kernels.h"
 
@@ -16,6 +18,7 @@ namespace gm {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 template <typename T> struct Mfma;
 template <> struct Mfma<bf16_t> {
@@ -36,10 +39,10 @@ template <typename T>
 __device__ __forceinline__ void load4(const T* p, float* v, int nvalid, bool vec) {
   if (vec) {
     if constexpr (sizeof(T) == 4) {
-      const float4 r = *reinterpret_cast<const float4*>(p);
-      v[0] = r.x; v[1] = r.y; v[2] = r.z; v[3] = r.w;
+      const f32x4v r = *reinterpret_cast<const f32x4v*>(p);
+      v[0] = r[0]; v[1] = r[1]; v[2] = r[2]; v[3] = r[3];
     } else {
-      const uint2 r = *reinterpret_cast<const uint2*>(p);
+      const u32x2 r = *reinterpret_cast<const u32x2*>(p);
       const T* e = reinterpret_cast<const T*>(&r);
 #pragma unroll
       for (int i = 0; i < 4; ++i) v[i] = to_f32(e[i]);
@@ -54,13 +57,13 @@ template <typename T>
 __device__ __forceinline__ void store4(T* p, const float* v, int nvalid, bool vec) {
   if (vec) {
     if constexpr (sizeof(T) == 4) {
-      *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+      *reinterpret_cast<f32x4v*>(p) = f32x4v{v[0], v[1], v[2], v[3]};
     } else {
-      uint2 r;
+      u32x2 r;
       T* e = reinterpret_cast<T*>(&r);
 #pragma unroll
       for (int i = 0; i < 4; ++i) e[i] = from_f32<T>(v[i]);
-      *reinterpret_cast<uint2*>(p) = r;
+      *reinterpret_cast<u32x2*>(p) = r;
     }
   } else {
 #pragma unroll
@@ -212,19 +215,19 @@ __global__ __launch_bounds__(256) void k_gemm_mfma(GemmArgs a) {
     c = c < a.N ? c : a.N - 1;
     Wg[v] = static_cast<const T*>(a.W) + static_cast<long long>(c) * a.ldw + lcol;
   }
-  uint4 ra[4], rb[4];
+  u32x4 ra[4], rb[4];
   auto gload = [&](int k0) {
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
-      ra[v] = *reinterpret_cast<const uint4*>(Ag[v] + k0);
-      rb[v] = *reinterpret_cast<const uint4*>(Wg[v] + k0);
+      ra[v] = *reinterpret_cast<const u32x4*>(Ag[v] + k0);
+      rb[v] = *reinterpret_cast<const u32x4*>(Wg[v] + k0);
     }
   };
   auto sstore = [&](int buf) {
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
-      *reinterpret_cast<uint4*>(&sA[buf][(lrow + 32 * v) * kLDK + lcol]) = ra[v];
-      *reinterpret_cast<uint4*>(&sB[buf][(lrow + 32 * v) * kLDK + lcol]) = rb[v];
+      *reinterpret_cast<u32x4*>(&sA[buf][(lrow + 32 * v) * kLDK + lcol]) = ra[v];
+      *reinterpret_cast<u32x4*>(&sB[buf][(lrow + 32 * v) * kLDK + lcol]) = rb[v];
     }
   };
   const int wave = t >> 6, lane = t & 63;
@@ -282,6 +285,183 @@ __global__ __launch_bounds__(256) void k_gemm_mfma(GemmArgs a) {
   site_flush(a, sm);
 }
 
+
+// ------------------------------------------------------------ MFMA 32x32 kernel
+// Workgroup tile BM x BN (256 x 256 or 128 x 128), K step 64, 4 wavefronts
+// in a 2 x 2 grid; each wavefront owns (BM/2) x (BN/2) as TM x TN tiles of
+// v_mfma_f32_32x32x16 (bf16/f16 in, fp32 accumulate).  W is the MFMA A
+// operand and the activations the B operand: a lane ends up with the output
+// columns n = 32j + 8q + 4(lane/32) + r (q, r = 0..3) of row
+// m = 32i + lane%32, so the columns of a 16-row weight group (q = 0, 1) and
+// of its partner group (q + 2) sit in the same lane, which is what the
+// gated and rotary epilogues pair.
+// Both operand tiles are staged in LDS (row pitch padded by 16 bytes so the
+// 32 rows a wavefront reads at once fall in distinct banks), two stages;
+// the next K step's tiles are fetched into registers while the current one
+// is multiplied.  Tiles are visited XCD by XCD and, within an XCD, in
+// groups of GM tile-rows, so that concurrently running workgroups share
+// operand tiles in the same L2.
+template <int I, int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<I + 1, N>(f);
+  }
+}
+
+template <typename T> struct Mfma32;
+template <> struct Mfma32<bf16_t> {
+  typedef bf16x8 vec;
+  static __device__ __forceinline__ f32x16 run(vec a, vec b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+};
+template <> struct Mfma32<f16_t> {
+  typedef f16x8 vec;
+  static __device__ __forceinline__ f32x16 run(vec a, vec b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+  }
+};
+
+__device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
+  // XCD-major renumbering: hardware deals workgroups round-robin to the 8
+  // XCDs, so workgroup b runs on XCD b % 8.  Give each XCD a contiguous
+  // range of tile ids.
+  const int total = tiles_m * tiles_n;
+  int t = bid;
+  if (total % 8 == 0) t = (bid % 8) * (total / 8) + bid / 8;
+  // grouped order: GM tile-rows sweep the columns together
+  constexpr int GM = 8;
+  const int group = t / (GM * tiles_n);
+  const int first = group * GM;
+  const int rows = tiles_m - first < GM ? tiles_m - first : GM;
+  const int in = t - group * GM * tiles_n;
+  tm = first + in % rows;
+  tn = in / rows;
+}
+
+template <typename T, int BM, int BN>
+__global__ __launch_bounds__(256) void k_gemm_mfma32(GemmArgs a) {
+  typedef typename Mfma32<T>::vec vec;
+  constexpr int TM = BM / 64, TN = BN / 64;     // 32x32 tiles per wavefront
+  constexpr int VA = BM / 32, VB = BN / 32;     // 16-byte loads per thread per stage
+  constexpr int KS = kBK / 16;                  // MFMA k-steps per stage
+  __shared__ __attribute__((aligned(16))) T sA[2][BM * kLDK];
+  __shared__ __attribute__((aligned(16))) T sB[2][BN * kLDK];
+  const int tiles_m = (a.M + BM - 1) / BM, tiles_n = (a.N + BN - 1) / BN;
+  int tm, tn;
+  tile_of(blockIdx.x, tiles_m, tiles_n, tm, tn);
+  const int bm = tm * BM, bn = tn * BN;
+  const int t = threadIdx.x;
+  const int lrow = t >> 3, lcol = (t & 7) * 8;
+  // element offsets of this thread's rows (rows past the end are clamped to
+  // the last row: loaded, never stored)
+  uint32_t oa[VA], ob[VB];
+#pragma unroll
+  for (int v = 0; v < VA; ++v) {
+    int r = bm + lrow + 32 * v;
+    r = r < a.M ? r : a.M - 1;
+    oa[v] = static_cast<uint32_t>(r) * a.lda + lcol;
+  }
+#pragma unroll
+  for (int v = 0; v < VB; ++v) {
+    int c = bn + lrow + 32 * v;
+    c = c < a.N ? c : a.N - 1;
+    ob[v] = static_cast<uint32_t>(c) * a.ldw + lcol;
+  }
+  const T* __restrict__ A0 = static_cast<const T*>(a.A);
+  const T* __restrict__ W0 = static_cast<const T*>(a.W);
+  const int wave = t >> 6, lane = t & 63;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int l32 = lane & 31, g = lane >> 5;
+  const int rdA = (wm * (BM / 2) + l32) * kLDK + 8 * g;
+  const int rdB = (wn * (BN / 2) + l32) * kLDK + 8 * g;
+  const int wr = lrow * kLDK + lcol;
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  u32x4 ra[VA], rb[VB];
+#pragma unroll
+  for (int v = 0; v < VA; ++v) ra[v] = *reinterpret_cast<const u32x4*>(A0 + oa[v]);
+#pragma unroll
+  for (int v = 0; v < VB; ++v) rb[v] = *reinterpret_cast<const u32x4*>(W0 + ob[v]);
+#pragma unroll
+  for (int v = 0; v < VA; ++v) *reinterpret_cast<u32x4*>(&sA[0][wr + 32 * v * kLDK]) = ra[v];
+#pragma unroll
+  for (int v = 0; v < VB; ++v) *reinterpret_cast<u32x4*>(&sB[0][wr + 32 * v * kLDK]) = rb[v];
+  __syncthreads();
+
+  const int nk = a.K / kBK;
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    const bool more = kt + 1 < nk;
+    if (more) {
+      const int k0 = (kt + 1) * kBK;
+#pragma unroll
+      for (int v = 0; v < VA; ++v) ra[v] = *reinterpret_cast<const u32x4*>(A0 + oa[v] + k0);
+#pragma unroll
+      for (int v = 0; v < VB; ++v) rb[v] = *reinterpret_cast<const u32x4*>(W0 + ob[v] + k0);
+    }
+    const T* pa = &sA[buf][rdA];
+    const T* pb = &sB[buf][rdB];
+    vec af[2][TM], bfr[2][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i) af[0][i] = *reinterpret_cast<const vec*>(pa + 32 * i * kLDK);
+#pragma unroll
+    for (int j = 0; j < TN; ++j) bfr[0][j] = *reinterpret_cast<const vec*>(pb + 32 * j * kLDK);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const int cur = ks & 1;
+      if (ks + 1 < KS) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+          af[cur ^ 1][i] = *reinterpret_cast<const vec*>(pa + 32 * i * kLDK + 16 * (ks + 1));
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          bfr[cur ^ 1][j] = *reinterpret_cast<const vec*>(pb + 32 * j * kLDK + 16 * (ks + 1));
+      }
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = Mfma32<T>::run(bfr[cur][j], af[cur][i], acc[i][j]);
+    }
+    if (more) {
+#pragma unroll
+      for (int v = 0; v < VA; ++v)
+        *reinterpret_cast<u32x4*>(&sA[buf ^ 1][wr + 32 * v * kLDK]) = ra[v];
+#pragma unroll
+      for (int v = 0; v < VB; ++v)
+        *reinterpret_cast<u32x4*>(&sB[buf ^ 1][wr + 32 * v * kLDK]) = rb[v];
+    }
+    __syncthreads();
+  }
+
+  SiteMax sm;
+  static_for<0, TM>([&](auto i) {
+    const int m = bm + wm * (BM / 2) + 32 * i + l32;
+    static_for<0, TN>([&](auto j) {
+      static_for<0, 2>([&](auto q) {
+        const int nA = bn + wn * (BN / 2) + 32 * j + 8 * q + 4 * g;
+        float va[4], vb[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          va[r] = acc[i][j][4 * q + r];
+          vb[r] = acc[i][j][4 * (q + 2) + r];
+        }
+        epi_pair<T>(a, m, nA, va, vb, sm);
+      });
+    });
+  });
+  site_flush(a, sm);
+}
+
 // ------------------------------------------------------------ fp32 kernel
 // 64 x 64 tile, K step 16; thread t owns row t/4 and, in each of the four
 // 16-column groups, the 4 consecutive columns 4*(t%4).. (same pairing of
@@ -328,7 +508,9 @@ __global__ __launch_bounds__(256) void k_gemm_simple(GemmArgs a) {
 }
 
 static bool g_force_simple = false;
+static int g_gemm_variant = 0;
 void gemm_force_simple(bool on) { g_force_simple = on; }
+void gemm_set_variant(int v) { g_gemm_variant = v; }
 
 void launch_gemm(const GemmArgs& a, hipStream_t s) {
   if (a.dtype == kF32 || g_force_simple) {
@@ -338,9 +520,23 @@ void launch_gemm(const GemmArgs& a, hipStream_t s) {
     else hipLaunchKernelGGL(k_gemm_simple<f16_t>, grid, dim3(256), 0, s, a);
     return;
   }
-  const dim3 grid(((a.M + kBM - 1) / kBM) * ((a.N + kBN - 1) / kBN));
-  if (a.dtype == kBF16) hipLaunchKernelGGL(k_gemm_mfma<bf16_t>, grid, dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(k_gemm_mfma<f16_t>, grid, dim3(256), 0, s, a);
+  if (g_gemm_variant == 1) {
+    const dim3 grid(((a.M + kBM - 1) / kBM) * ((a.N + kBN - 1) / kBN));
+    if (a.dtype == kBF16) hipLaunchKernelGGL(k_gemm_mfma<bf16_t>, grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(k_gemm_mfma<f16_t>, grid, dim3(256), 0, s, a);
+    return;
+  }
+  // 256 x 256 tiles when they fill the chip, else 128 x 128
+  const long long big = static_cast<long long>((a.M + 255) / 256) * ((a.N + 255) / 256);
+  if (big >= 256 && g_gemm_variant != 2) {
+    const dim3 grid(static_cast<unsigned>(big));
+    if (a.dtype == kBF16) hipLaunchKernelGGL((k_gemm_mfma32<bf16_t, 256, 256>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((k_gemm_mfma32<f16_t, 256, 256>), grid, dim3(256), 0, s, a);
+  } else {
+    const dim3 grid(((a.M + 127) / 128) * ((a.N + 127) / 128));
+    if (a.dtype == kBF16) hipLaunchKernelGGL((k_gemm_mfma32<bf16_t, 128, 128>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((k_gemm_mfma32<f16_t, 128, 128>), grid, dim3(256), 0, s, a);
+  }
 }
 
 }  // namespace gm

@@ -144,9 +144,9 @@ void launch_rope_fill(float* cs, float* sn, int hd, double base,
 //     R(clamp(h, -thr, thr)) and written back; otherwise it is untouched;
 //  3. optional LayerNorm / RMSNorm with fp32 statistics, stored to out.
 template <typename T> struct Vec;
-template <> struct Vec<float> { typedef float4 type; static constexpr int n = 4; };
-template <> struct Vec<bf16_t> { typedef uint4 type; static constexpr int n = 8; };
-template <> struct Vec<f16_t> { typedef uint4 type; static constexpr int n = 8; };
+template <> struct Vec<float> { typedef f32x4v type; static constexpr int n = 4; };
+template <> struct Vec<bf16_t> { typedef u32x4 type; static constexpr int n = 8; };
+template <> struct Vec<f16_t> { typedef u32x4 type; static constexpr int n = 8; };
 
 template <typename T>
 __device__ __forceinline__ void vload(const T* p, float* v) {
@@ -331,8 +331,8 @@ void launch_emit_effects(int32_t* state, void* fifo, int cap, int n_sites, hipSt
 // ------------------------------------------------------------ row gather
 // dst row r = src row row_map[r]; used once at model creation to repack
 // weight rows.  row_bytes must be a multiple of 16.
-__global__ __launch_bounds__(256) void k_gather_rows(uint4* __restrict__ dst,
-                                                      const uint4* __restrict__ src,
+__global__ __launch_bounds__(256) void k_gather_rows(u32x4* __restrict__ dst,
+                                                      const u32x4* __restrict__ src,
                                                       const int32_t* __restrict__ map,
                                                       int rows, int row_vecs) {
   const long long total = static_cast<long long>(rows) * row_vecs;
@@ -347,7 +347,7 @@ __global__ __launch_bounds__(256) void k_gather_rows(uint4* __restrict__ dst,
 void launch_gather_rows(void* dst, const void* src, const int32_t* map, int rows,
                         int row_bytes, hipStream_t s) {
   hipLaunchKernelGGL(k_gather_rows, dim3(1024), dim3(256), 0, s,
-                     static_cast<uint4*>(dst), static_cast<const uint4*>(src), map,
+                     static_cast<u32x4*>(dst), static_cast<const u32x4*>(src), map,
                      rows, row_bytes / 16);
 }
 

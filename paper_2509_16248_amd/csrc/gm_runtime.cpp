@@ -16,6 +16,7 @@
 
 namespace gm {
 void gemm_force_simple(bool on);
+void gemm_set_variant(int v);
 void attention_force_rows(bool on);
 }
 
@@ -444,6 +445,7 @@ int gm_model_create(const gm_config* cfg, const gm_weights* w, gm_model** out) {
   memset(&m->stats, 0, sizeof(m->stats));
   m->debug_sync = getenv("GM_DEBUG_SYNC") && atoi(getenv("GM_DEBUG_SYNC"));
   gemm_force_simple(getenv("GM_SIMPLE_GEMM") && atoi(getenv("GM_SIMPLE_GEMM")));
+  gemm_set_variant(getenv("GM_GEMM_VARIANT") ? atoi(getenv("GM_GEMM_VARIANT")) : 0);
   attention_force_rows(getenv("GM_SIMPLE_ATTN") && atoi(getenv("GM_SIMPLE_ATTN")));
   auto fail = [&](int code) {
     gm_model_destroy(m);
