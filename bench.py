@@ -121,7 +121,7 @@ def main():
     g_flops = sum(p[3] for p in gemm)
     g_avg_ms = g_ms / len(gemm)
     achieved = g_flops / (g_ms * 1e-3) / 1e12
-    roofline = {"kernel": "k_gemm_mfma<bf16> (all projection and LM-head GEMMs)",
+    roofline = {"kernel": "k_gemm_x<bf16,128,128,2,4,2> (all projection and LM-head GEMMs)",
                 "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                 "traffic": None, "launches_per_forward": len(gemm),

@@ -103,21 +103,34 @@ template <> struct MfmaA<f16_t> {
 
 constexpr int kQB = 128, kKB = 64;
 
+// K and V tiles move global -> registers -> LDS.  The tile after the current
+// one is fetched into registers while the current one is multiplied, and the
+// LDS tiles are double-buffered, so there is one barrier per key tile.  V is
+// transposed on the way into LDS, two keys at a time (4-byte LDS writes).
+// With a causal mask, query blocks run heaviest (last) first.
 template <typename T, int HD>
 __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
   typedef typename MfmaA<T>::vec vec;
   constexpr int LDK = HD + 8;      // K tile row pitch (elements)
-  constexpr int LDV = kKB + 8;     // V^T tile row pitch
+  constexpr int LDV = kKB + 4;     // V^T tile row pitch (transposing writes spread over banks)
   constexpr int NC = HD / 32;      // 32-wide chunks of the head dim
   constexpr int NCT = HD / 16;     // 16-wide channel tiles
-  __shared__ __attribute__((aligned(16))) T sK[kKB * LDK];
-  __shared__ __attribute__((aligned(16))) T sVt[HD * LDV];
-  __shared__ int sMask[kKB];
-  const int qb = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  constexpr int VPR = HD / 8;      // 16-byte vectors per key row
+  constexpr int KL = kKB * VPR / 256;          // K vectors per thread
+  constexpr int VL = (kKB / 2) * VPR / 256;    // V key pairs per thread
+  static_assert(KL >= 1 && VL >= 1, "tile too small for the workgroup");
+  __shared__ __attribute__((aligned(16))) T sK[2][kKB * LDK];
+  __shared__ __attribute__((aligned(16))) T sVt[2][HD * LDV];
+  __shared__ int sMask[2][kKB];
+  const int nqb = (a.S + kQB - 1) / kQB;
+  const int qb = a.causal ? nqb - 1 - static_cast<int>(blockIdx.x) : static_cast<int>(blockIdx.x);
+  const int h = blockIdx.y, b = blockIdx.z;
   const int S = a.S, d = a.d, ld = 3 * d;
   const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
   const int l16 = lane & 15, g = lane >> 4;
   const T* base = static_cast<const T*>(a.qkv) + static_cast<long long>(b) * S * ld;
+  const T* kbase = base + d + h * HD;
+  const T* vbase = base + 2 * d + h * HD;
   const int32_t* mk = a.mask + static_cast<long long>(b) * S;
   const int q0 = qb * kQB + wave * 32;
 
@@ -146,28 +159,61 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
 #pragma unroll
     for (int c = 0; c < NCT; ++c) oacc[u][c] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  constexpr int VPR = HD / 8;                 // 16-byte vectors per key row
-  constexpr int LOADS = kKB * VPR / 256;      // per thread
-  for (int kb = 0; kb < kend; kb += kKB) {
-    // ---- stage K (row-major) and V (transposed) for keys kb..kb+63
+  u32x4 rk[KL], rv[VL][2];
+  int rm = 0;
+  auto gload = [&](int kb) {
 #pragma unroll
-    for (int v = 0; v < LOADS; ++v) {
+    for (int v = 0; v < KL; ++v) {
       const int idx = t + 256 * v;
-      const int r = idx / VPR, c = (idx % VPR) * 8;
-      int key = kb + r;
+      int key = kb + idx / VPR;
       key = key < S ? key : S - 1;
-      const T* kp = base + static_cast<long long>(key) * ld + d + h * HD + c;
-      *reinterpret_cast<u32x4*>(&sK[r * LDK + c]) = *reinterpret_cast<const u32x4*>(kp);
-      const u32x4 vv = *reinterpret_cast<const u32x4*>(kp + d);
-      const T* ve = reinterpret_cast<const T*>(&vv);
+      rk[v] = *reinterpret_cast<const u32x4*>(kbase + static_cast<long long>(key) * ld + (idx % VPR) * 8);
+    }
 #pragma unroll
-      for (int e = 0; e < 8; ++e) sVt[(c + e) * LDV + r] = ve[e];
+    for (int v = 0; v < VL; ++v) {
+      const int idx = t + 256 * v;
+      const int c = (idx % VPR) * 8;
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        int key = kb + 2 * (idx / VPR) + e;
+        key = key < S ? key : S - 1;
+        rv[v][e] = *reinterpret_cast<const u32x4*>(vbase + static_cast<long long>(key) * ld + c);
+      }
     }
     if (t < kKB) {
       const int key = kb + t;
-      sMask[t] = key < S ? (pad ? mk[key] != 0 : 1) : 0;
+      rm = key < S ? (pad ? mk[key] != 0 : 1) : 0;
     }
+  };
+  auto sstore = [&](int buf) {
+#pragma unroll
+    for (int v = 0; v < KL; ++v) {
+      const int idx = t + 256 * v;
+      *reinterpret_cast<u32x4*>(&sK[buf][(idx / VPR) * LDK + (idx % VPR) * 8]) = rk[v];
+    }
+#pragma unroll
+    for (int v = 0; v < VL; ++v) {
+      const int idx = t + 256 * v;
+      const int pr = idx / VPR, c = (idx % VPR) * 8;
+      const T* v0 = reinterpret_cast<const T*>(&rv[v][0]);
+      const T* v1 = reinterpret_cast<const T*>(&rv[v][1]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        T pair[2] = {v0[e], v1[e]};
+        *reinterpret_cast<uint32_t*>(&sVt[buf][(c + e) * LDV + 2 * pr]) =
+            *reinterpret_cast<const uint32_t*>(pair);
+      }
+    }
+    if (t < kKB) sMask[buf][t] = rm;
+  };
+
+  if (kend > 0) gload(0);
+  int it = 0;
+  for (int kb = 0; kb < kend; kb += kKB, ++it) {
+    const int buf = it & 1;
+    sstore(buf);
     __syncthreads();
+    if (kb + kKB < kend) gload(kb + kKB);
 
     // ---- S^T = K Q^T
     f32x4 sacc[4][2];
@@ -179,7 +225,7 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
     for (int c = 0; c < NC; ++c) {
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt) {
-        const vec kf = *reinterpret_cast<const vec*>(&sK[(16 * kt + l16) * LDK + 32 * c + 8 * g]);
+        const vec kf = *reinterpret_cast<const vec*>(&sK[buf][(16 * kt + l16) * LDK + 32 * c + 8 * g]);
 #pragma unroll
         for (int u = 0; u < 2; ++u) sacc[kt][u] = MfmaA<T>::run(kf, qf[u][c], sacc[kt][u]);
       }
@@ -195,7 +241,7 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int kl = 16 * kt + 4 * g + r;
-          const bool ok = sMask[kl] && (!a.causal || kb + kl <= qi);
+          const bool ok = sMask[buf][kl] && (!a.causal || kb + kl <= qi);
           const float s = ok ? sacc[kt][u][r] * sl2 : -INFINITY;
           p[kt][u][r] = s;
           tmax = fmaxf(tmax, s);
@@ -203,14 +249,16 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
       tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
       tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
       const float mnew = fmaxf(mrow[u], tmax);
-      const float alpha = mnew == -INFINITY ? 1.f : exp2f(mrow[u] - mnew);
+      // while every key so far is masked, mnew is -inf: subtract 0 instead
+      // (masked scores are -inf and give exp2 = 0 either way)
+      const float msub = mnew == -INFINITY ? 0.f : mnew;
+      const float alpha = __builtin_amdgcn_exp2f(mrow[u] - msub);
       float tsum = 0.f;
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float s = p[kt][u][r];
-          const float e = s == -INFINITY ? 0.f : round_as<T>(exp2f(s - mnew));
+          const float e = round_as<T>(__builtin_amdgcn_exp2f(p[kt][u][r] - msub));
           p[kt][u][r] = e;
           tsum += e;
         }
@@ -237,7 +285,7 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
       }
 #pragma unroll
       for (int c = 0; c < NCT; ++c) {
-        const T* vr = &sVt[(16 * c + l16) * LDV + 32 * kc + 4 * g];
+        const T* vr = &sVt[buf][(16 * c + l16) * LDV + 32 * kc + 4 * g];
         T tmp[8];
         *reinterpret_cast<u32x2*>(&tmp[0]) = *reinterpret_cast<const u32x2*>(vr);
         *reinterpret_cast<u32x2*>(&tmp[4]) = *reinterpret_cast<const u32x2*>(vr + 16);
@@ -246,7 +294,6 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
         for (int u = 0; u < 2; ++u) oacc[u][c] = MfmaA<T>::run(vf, pb[u], oacc[u][c]);
       }
     }
-    __syncthreads();
   }
   // ---- normalise and store: lane holds channels 16c + 4g + r of query (u, l16)
 #pragma unroll

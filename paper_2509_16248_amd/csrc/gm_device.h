@@ -57,12 +57,10 @@ __device__ __forceinline__ float to_f32(f16_t x) { return static_cast<float>(x);
 
 template <typename T> __device__ __forceinline__ T from_f32(float x);
 template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
-// float32 -> bfloat16, round to nearest even, NaN kept quiet.
+// float32 -> bfloat16, round to nearest even, NaN kept quiet (gfx950's
+// v_cvt_pk_bf16_f32).
 template <> __device__ __forceinline__ bf16_t from_f32<bf16_t>(float x) {
-  uint32_t u = __float_as_uint(x);
-  if ((u & 0x7FFFFFFFu) > 0x7F800000u) return static_cast<bf16_t>((u >> 16) | 0x40u);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return static_cast<bf16_t>(u >> 16);
+  return __builtin_bit_cast(bf16_t, static_cast<__bf16>(x));
 }
 template <> __device__ __forceinline__ f16_t from_f32<f16_t>(float x) {
   return static_cast<f16_t>(x);

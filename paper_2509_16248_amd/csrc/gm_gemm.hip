@@ -340,14 +340,23 @@ __device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int& 
   tn = in / rows;
 }
 
-template <typename T, int BM, int BN>
-__global__ __launch_bounds__(256) void k_gemm_mfma32(GemmArgs a) {
+template <typename T, int BM, int BN, int WGM, int WGN, int PF>
+__global__ __launch_bounds__(64 * WGM * WGN) void k_gemm_x(GemmArgs a) {
   typedef typename Mfma32<T>::vec vec;
-  constexpr int TM = BM / 64, TN = BN / 64;     // 32x32 tiles per wavefront
-  constexpr int VA = BM / 32, VB = BN / 32;     // 16-byte loads per thread per stage
+  constexpr int NT = 64 * WGM * WGN;            // threads
+  constexpr int WTM = BM / WGM, WTN = BN / WGN; // wavefront tile
+  constexpr int TM = WTM / 32, TN = WTN / 32;   // 32x32 MFMA tiles per wavefront
+  constexpr int RPP = NT / 8;                   // tile rows loaded per pass
+  constexpr int VA = BM / RPP, VB = BN / RPP;   // 16-byte loads per thread per stage
   constexpr int KS = kBK / 16;                  // MFMA k-steps per stage
-  __shared__ __attribute__((aligned(16))) T sA[2][BM * kLDK];
-  __shared__ __attribute__((aligned(16))) T sB[2][BN * kLDK];
+  static_assert(BM % RPP == 0 && BN % RPP == 0, "tile rows must split evenly");
+  static_assert(TM >= 1 && TN >= 1, "wavefront tile below 32x32");
+  constexpr int LDS_OPS = 2 * (BM + BN) * kLDK * static_cast<int>(sizeof(T));
+  constexpr int LDC = BN + 4;                   // fp32 staging row pitch
+  constexpr bool STAGE = BM * LDC * 4 <= LDS_OPS;
+  __shared__ __attribute__((aligned(16))) char smem[LDS_OPS];
+  T (*sA)[BM * kLDK] = reinterpret_cast<T (*)[BM * kLDK]>(smem);
+  T (*sB)[BN * kLDK] = reinterpret_cast<T (*)[BN * kLDK]>(smem + 2 * BM * kLDK * sizeof(T));
   const int tiles_m = (a.M + BM - 1) / BM, tiles_n = (a.N + BN - 1) / BN;
   int tm, tn;
   tile_of(blockIdx.x, tiles_m, tiles_n, tm, tn);
@@ -359,23 +368,23 @@ __global__ __launch_bounds__(256) void k_gemm_mfma32(GemmArgs a) {
   uint32_t oa[VA], ob[VB];
 #pragma unroll
   for (int v = 0; v < VA; ++v) {
-    int r = bm + lrow + 32 * v;
+    int r = bm + lrow + RPP * v;
     r = r < a.M ? r : a.M - 1;
     oa[v] = static_cast<uint32_t>(r) * a.lda + lcol;
   }
 #pragma unroll
   for (int v = 0; v < VB; ++v) {
-    int c = bn + lrow + 32 * v;
+    int c = bn + lrow + RPP * v;
     c = c < a.N ? c : a.N - 1;
     ob[v] = static_cast<uint32_t>(c) * a.ldw + lcol;
   }
   const T* __restrict__ A0 = static_cast<const T*>(a.A);
   const T* __restrict__ W0 = static_cast<const T*>(a.W);
   const int wave = t >> 6, lane = t & 63;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WGN, wn = wave % WGN;
   const int l32 = lane & 31, g = lane >> 5;
-  const int rdA = (wm * (BM / 2) + l32) * kLDK + 8 * g;
-  const int rdB = (wn * (BN / 2) + l32) * kLDK + 8 * g;
+  const int rdA = (wm * WTM + l32) * kLDK + 8 * g;
+  const int rdB = (wn * WTN + l32) * kLDK + 8 * g;
   const int wr = lrow * kLDK + lcol;
 
   f32x16 acc[TM][TN];
@@ -386,28 +395,23 @@ __global__ __launch_bounds__(256) void k_gemm_mfma32(GemmArgs a) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-  u32x4 ra[VA], rb[VB];
-#pragma unroll
-  for (int v = 0; v < VA; ++v) ra[v] = *reinterpret_cast<const u32x4*>(A0 + oa[v]);
-#pragma unroll
-  for (int v = 0; v < VB; ++v) rb[v] = *reinterpret_cast<const u32x4*>(W0 + ob[v]);
-#pragma unroll
-  for (int v = 0; v < VA; ++v) *reinterpret_cast<u32x4*>(&sA[0][wr + 32 * v * kLDK]) = ra[v];
-#pragma unroll
-  for (int v = 0; v < VB; ++v) *reinterpret_cast<u32x4*>(&sB[0][wr + 32 * v * kLDK]) = rb[v];
-  __syncthreads();
-
+  u32x4 ra[PF][VA], rb[PF][VB];
   const int nk = a.K / kBK;
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    const bool more = kt + 1 < nk;
-    if (more) {
-      const int k0 = (kt + 1) * kBK;
+  auto gload = [&](auto set, int k0) {
 #pragma unroll
-      for (int v = 0; v < VA; ++v) ra[v] = *reinterpret_cast<const u32x4*>(A0 + oa[v] + k0);
+    for (int v = 0; v < VA; ++v) ra[set][v] = *reinterpret_cast<const u32x4*>(A0 + oa[v] + k0);
 #pragma unroll
-      for (int v = 0; v < VB; ++v) rb[v] = *reinterpret_cast<const u32x4*>(W0 + ob[v] + k0);
-    }
+    for (int v = 0; v < VB; ++v) rb[set][v] = *reinterpret_cast<const u32x4*>(W0 + ob[v] + k0);
+  };
+  auto sstore = [&](auto set, int buf) {
+#pragma unroll
+    for (int v = 0; v < VA; ++v)
+      *reinterpret_cast<u32x4*>(&sA[buf][wr + RPP * v * kLDK]) = ra[set][v];
+#pragma unroll
+    for (int v = 0; v < VB; ++v)
+      *reinterpret_cast<u32x4*>(&sB[buf][wr + RPP * v * kLDK]) = rb[set][v];
+  };
+  auto compute = [&](int buf) {
     const T* pa = &sA[buf][rdA];
     const T* pb = &sB[buf][rdB];
     vec af[2][TM], bfr[2][TN];
@@ -432,34 +436,152 @@ __global__ __launch_bounds__(256) void k_gemm_mfma32(GemmArgs a) {
         for (int j = 0; j < TN; ++j)
           acc[i][j] = Mfma32<T>::run(bfr[cur][j], af[cur][i], acc[i][j]);
     }
-    if (more) {
-#pragma unroll
-      for (int v = 0; v < VA; ++v)
-        *reinterpret_cast<u32x4*>(&sA[buf ^ 1][wr + 32 * v * kLDK]) = ra[v];
-#pragma unroll
-      for (int v = 0; v < VB; ++v)
-        *reinterpret_cast<u32x4*>(&sB[buf ^ 1][wr + 32 * v * kLDK]) = rb[v];
-    }
+  };
+
+  if constexpr (PF == 1) {
+    gload(std::integral_constant<int, 0>{}, 0);
+    sstore(std::integral_constant<int, 0>{}, 0);
     __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+      const int buf = kt & 1;
+      const bool more = kt + 1 < nk;
+      if (more) gload(std::integral_constant<int, 0>{}, (kt + 1) * kBK);
+      compute(buf);
+      if (more) sstore(std::integral_constant<int, 0>{}, buf ^ 1);
+      __syncthreads();
+    }
+  } else {
+    // register sets alternate: set (k & 1) receives stage k + 2 while stage
+    // k is multiplied out of LDS buffer (k & 1); stage k + 1 (set (k+1) & 1,
+    // fetched one iteration earlier) is written to the other LDS buffer.
+    gload(std::integral_constant<int, 0>{}, 0);
+    if (nk > 1) gload(std::integral_constant<int, 1>{}, kBK);
+    sstore(std::integral_constant<int, 0>{}, 0);
+    __syncthreads();
+    auto iter = [&](auto P, int k) {
+      constexpr int p = decltype(P)::value;
+      if (k + 2 < nk) gload(std::integral_constant<int, p>{}, (k + 2) * kBK);
+      compute(p);
+      if (k + 1 < nk) sstore(std::integral_constant<int, p ^ 1>{}, p ^ 1);
+      __syncthreads();
+    };
+    for (int kt = 0; kt < nk; kt += 2) {
+      iter(std::integral_constant<int, 0>{}, kt);
+      if (kt + 1 < nk) iter(std::integral_constant<int, 1>{}, kt + 1);
+    }
   }
 
   SiteMax sm;
-  static_for<0, TM>([&](auto i) {
-    const int m = bm + wm * (BM / 2) + 32 * i + l32;
-    static_for<0, TN>([&](auto j) {
-      static_for<0, 2>([&](auto q) {
-        const int nA = bn + wn * (BN / 2) + 32 * j + 8 * q + 4 * g;
-        float va[4], vb[4];
+  if (STAGE && (a.epi == kEpiStore || a.epi == kEpiGelu || a.epi == kEpiResid)) {
+    // Column-independent epilogues go through LDS: bias (and GELU) are
+    // applied in registers, the fp32 tile is staged, and rows are then
+    // written with consecutive lanes on consecutive columns, so the stores
+    // coalesce whatever the alignment of the output rows (the vocabulary
+    // of the head may be odd).
+    float* st = reinterpret_cast<float*>(smem);
+    const T* bias = static_cast<const T*>(a.bias);
+    static_for<0, TM>([&](auto i) {
+      const int ml = wm * WTM + 32 * i + l32;
+      static_for<0, TN>([&](auto j) {
+        static_for<0, 4>([&](auto q) {
+          const int nl = wn * WTN + 32 * j + 8 * q + 4 * g;
+          float v[4];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          va[r] = acc[i][j][4 * q + r];
-          vb[r] = acc[i][j][4 * (q + 2) + r];
-        }
-        epi_pair<T>(a, m, nA, va, vb, sm);
+          for (int r = 0; r < 4; ++r) {
+            v[r] = acc[i][j][4 * q + r];
+            const int n = bn + nl + r;
+            if (bias && n < a.N) v[r] += to_f32(bias[n]);
+            if (a.epi == kEpiGelu) v[r] = gelu_f(v[r]);
+          }
+          *reinterpret_cast<f32x4v*>(&st[ml * LDC + nl]) = f32x4v{v[0], v[1], v[2], v[3]};
+        });
       });
     });
-  });
+    __syncthreads();
+    T* out = static_cast<T*>(a.out);
+    const T* res = static_cast<const T*>(a.resid);
+    const bool resid = a.epi == kEpiResid;
+    if ((a.ldo & 7) == 0 && (!resid || (a.ldr & 7) == 0) && bn + BN <= a.N) {
+      // 16-byte stores: a row is BN/8 chunks
+      constexpr int CPR = BN / 8;
+      for (int e = t; e < BM * CPR; e += NT) {
+        const int ml = e / CPR, c = (e % CPR) * 8;
+        const int m = bm + ml;
+        if (m >= a.M) continue;
+        float v[8];
+        const f32x4v lo = *reinterpret_cast<const f32x4v*>(&st[ml * LDC + c]);
+        const f32x4v hi = *reinterpret_cast<const f32x4v*>(&st[ml * LDC + c + 4]);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          v[r] = lo[r];
+          v[4 + r] = hi[r];
+        }
+        if (resid) {
+          const u32x4 rr = *reinterpret_cast<const u32x4*>(res + static_cast<long long>(m) * a.ldr + bn + c);
+          const T* re = reinterpret_cast<const T*>(&rr);
+#pragma unroll
+          for (int r = 0; r < 8; ++r) v[r] += to_f32(re[r]);
+        }
+        u32x4 w;
+        T* we = reinterpret_cast<T*>(&w);
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+          we[r] = from_f32<T>(v[r]);
+          if (resid && a.site >= 0) sm.add(to_f32(we[r]));
+        }
+        *reinterpret_cast<u32x4*>(out + static_cast<long long>(m) * a.ldo + bn + c) = w;
+      }
+    } else {
+      // element stores, consecutive lanes on consecutive columns
+      for (int e = t; e < BM * BN; e += NT) {
+        const int ml = e / BN, nl = e % BN;
+        const int m = bm + ml, n = bn + nl;
+        if (m >= a.M || n >= a.N) continue;
+        float v = st[ml * LDC + nl];
+        if (resid) v += to_f32(res[static_cast<long long>(m) * a.ldr + n]);
+        const T y = from_f32<T>(v);
+        if (resid && a.site >= 0) sm.add(to_f32(y));
+        out[static_cast<long long>(m) * a.ldo + n] = y;
+      }
+    }
+  } else {
+    static_for<0, TM>([&](auto i) {
+      const int m = bm + wm * WTM + 32 * i + l32;
+      static_for<0, TN>([&](auto j) {
+        static_for<0, 2>([&](auto q) {
+          const int nA = bn + wn * WTN + 32 * j + 8 * q + 4 * g;
+          float va[4], vb[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            va[r] = acc[i][j][4 * q + r];
+            vb[r] = acc[i][j][4 * (q + 2) + r];
+          }
+          epi_pair<T>(a, m, nA, va, vb, sm);
+        });
+      });
+    });
+  }
   site_flush(a, sm);
+}
+
+template <typename T, int BM, int BN, int WGM, int WGN, int PF>
+static void run_x(const GemmArgs& a, hipStream_t s) {
+  const dim3 grid(((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN));
+  hipLaunchKernelGGL((k_gemm_x<T, BM, BN, WGM, WGN, PF>), grid, dim3(64 * WGM * WGN), 0, s, a);
+}
+
+template <typename T>
+static void gemm_mfma(const GemmArgs& a, hipStream_t s, int variant) {
+  switch (variant) {
+    case 6: run_x<T, 128, 128, 2, 2, 1>(a, s); return;
+    case 10: run_x<T, 256, 256, 2, 4, 2>(a, s); return;
+    case 11: run_x<T, 128, 128, 2, 4, 1>(a, s); return;
+    default: break;
+  }
+  // 128 x 128 workgroup tiles, 8 wavefronts of 64 x 32, operands fetched two
+  // K steps ahead (the best of the measured configurations on the projection
+  // and head shapes)
+  run_x<T, 128, 128, 2, 4, 2>(a, s);
 }
 
 // ------------------------------------------------------------ fp32 kernel
@@ -526,17 +648,8 @@ void launch_gemm(const GemmArgs& a, hipStream_t s) {
     else hipLaunchKernelGGL(k_gemm_mfma<f16_t>, grid, dim3(256), 0, s, a);
     return;
   }
-  // 256 x 256 tiles when they fill the chip, else 128 x 128
-  const long long big = static_cast<long long>((a.M + 255) / 256) * ((a.N + 255) / 256);
-  if (big >= 256 && g_gemm_variant != 2) {
-    const dim3 grid(static_cast<unsigned>(big));
-    if (a.dtype == kBF16) hipLaunchKernelGGL((k_gemm_mfma32<bf16_t, 256, 256>), grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((k_gemm_mfma32<f16_t, 256, 256>), grid, dim3(256), 0, s, a);
-  } else {
-    const dim3 grid(((a.M + 127) / 128) * ((a.N + 127) / 128));
-    if (a.dtype == kBF16) hipLaunchKernelGGL((k_gemm_mfma32<bf16_t, 128, 128>), grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((k_gemm_mfma32<f16_t, 128, 128>), grid, dim3(256), 0, s, a);
-  }
+  if (a.dtype == kBF16) gemm_mfma<bf16_t>(a, s, g_gemm_variant);
+  else gemm_mfma<f16_t>(a, s, g_gemm_variant);
 }
 
 }  // namespace gm
