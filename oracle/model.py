@@ -137,7 +137,8 @@ class OracleModel:
     # ---------------------------------------------------------------- forward
     def forward(self, ids: np.ndarray, mask: np.ndarray,
                 force: Optional[Dict] = None,
-                rows: Optional[List[int]] = None) -> OracleResult:
+                rows: Optional[List[int]] = None,
+                prefix: Optional[int] = None) -> OracleResult:
         """Run the original (graph-breaking) forward.
 
         ``force`` overrides the value a host-side predicate reads
@@ -147,6 +148,11 @@ class OracleModel:
         that the program evaluates over the whole batch (the padding branch)
         are still evaluated over the whole batch.  It is rejected for the
         fp16 clamp, whose predicate reads the residual of every sequence.
+        ``prefix`` (causal models only) computes the first ``prefix``
+        positions of each sequence; with a causal mask they depend on no later
+        position, so they equal those positions of the full forward.  The
+        predicates (padding branch, rotary cache size) still read the full
+        inputs, as the original program does.
         """
         c = self.cfg
         force = force or {}
@@ -196,8 +202,12 @@ class OracleModel:
             rows = list(range(B))
         if c.fp16_clamp and len(rows) != B:
             raise ValueError("the clamp predicate needs every sequence")
-        ids_r = ids[rows]
-        mask_r = mask[rows]
+        if prefix is not None:
+            if not c.causal or c.fp16_clamp:
+                raise ValueError("a prefix equals the full forward only for causal models")
+            S = min(S, prefix)
+        ids_r = ids[rows][:, :S]
+        mask_r = mask[rows][:, :S]
         Br = len(rows)
 
         # --- attention mask: causal and/or key padding (only if pad_any).

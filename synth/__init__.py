@@ -134,13 +134,20 @@ def preset(name: str, **overrides) -> ModelConfig:
 
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     """Encode float32 values as bfloat16 bit patterns (round to nearest even)."""
-    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
-    nan = np.isnan(np.asarray(x, dtype=np.float32))
-    # no uint32 overflow for non-NaN inputs: |u| <= 0xFF800000
-    r = ((u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)).astype(np.uint16)
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    u = x.view(np.uint32)
+    # r = (u + 0x7FFF + ((u >> 16) & 1)) >> 16, in place; no uint32 overflow
+    # for non-NaN inputs (|u| <= 0xFF800000)
+    r = np.right_shift(u, np.uint32(16))
+    np.bitwise_and(r, np.uint32(1), out=r)
+    np.add(r, np.uint32(0x7FFF), out=r)
+    np.add(r, u, out=r)
+    np.right_shift(r, np.uint32(16), out=r)
+    out = r.astype(np.uint16)
+    nan = np.isnan(x)
     if nan.any():
-        r = np.where(nan, np.uint16(0x7FC0), r)
-    return r
+        out[nan] = np.uint16(0x7FC0)
+    return out
 
 
 def encode(x: np.ndarray, dtype: str) -> np.ndarray:
@@ -247,9 +254,21 @@ class Weights:
         return n + sum(v.nbytes for L in self.layers for v in L.values())
 
 
-def make_weights(cfg: ModelConfig, seed: int = 1234) -> Weights:
-    return Weights(cfg, seed, make_global_weights(cfg, seed),
-                   [make_layer_weights(cfg, seed, l) for l in range(cfg.n_layers)])
+def make_weights(cfg: ModelConfig, seed: int = 1234, threads: Optional[int] = None) -> Weights:
+    """All weights; tensors are drawn on a thread pool (each has its own
+    generator, so the result does not depend on the thread count)."""
+    import concurrent.futures as cf
+    import os
+    tasks = [(k, None, shp) for k, shp in tensor_shapes(cfg).items()]
+    for l in range(cfg.n_layers):
+        tasks += [(k, l, shp) for k, shp in layer_shapes(cfg).items()]
+    n = threads or min(16, len(os.sched_getaffinity(0)))
+    with cf.ThreadPoolExecutor(max_workers=max(1, n)) as ex:
+        arrays = list(ex.map(lambda t: _draw(cfg, seed, t[0], t[1], t[2]), tasks))
+    glob, layers = {}, [dict() for _ in range(cfg.n_layers)]
+    for (k, l, _), a in zip(tasks, arrays):
+        (glob if l is None else layers[l])[k] = a
+    return Weights(cfg, seed, glob, layers)
 
 
 # ---------------------------------------------------------------- inputs

@@ -230,6 +230,21 @@ def test_row_subset_matches_full_batch():
     assert part.pad_any == full.pad_any
 
 
+def test_causal_prefix_matches_full_forward():
+    for cfg in (tiny_bf16_decoder(), tiny_rotary()):
+        w = synth.make_weights(cfg, 4)
+        ids, mask = inputs_with_pads(cfg, cfg.max_pad > 0)
+        full = OracleModel(cfg, w).forward(ids, mask)
+        part = OracleModel(cfg, w).forward(ids, mask, rows=[1], prefix=9)
+        assert part.pad_any == full.pad_any and part.regrow == full.regrow
+        assert part.cached_len == full.cached_len
+        np.testing.assert_allclose(part.logits_f64, full.logits_f64[[1], :9], rtol=0,
+                                   atol=1e-12 * np.abs(full.logits_f64).max())
+    with pytest.raises(ValueError):
+        OracleModel(tiny_encoder(), synth.make_weights(tiny_encoder(), 1)).forward(
+            *synth.make_inputs(tiny_encoder(), 0), prefix=4)
+
+
 # ------------------------------------------------------------ rotary cache
 
 def test_rotary_regrow_decisions_persist_across_calls():
