@@ -31,6 +31,20 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
+def measured_traffic():
+    """HBM bytes per GEMM launch from the committed rocprofv3 FETCH_SIZE /
+    WRITE_SIZE summary, if it was taken on the GEMM source as it is now."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "gemm_traffic_causal_lm_768.json")
+    src = os.path.join(ROOT, "paper_2509_16248_amd", "csrc", "gm_gemm.hip")
+    try:
+        rec = json.load(open(path))
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    except OSError:
+        return None
+    return rec["traffic_bytes_per_launch"] if rec.get("gm_gemm_hip_sha256") == sha else None
+
+
 def cpu_baseline(cfg, w, ids, mask, rows):
     """The oracle (float64 NumPy) on `rows` sequences of the same batch."""
     import numpy as np
@@ -124,7 +138,7 @@ def main():
     roofline = {"kernel": "k_gemm_x<bf16,128,128,2,4,2> (all projection and LM-head GEMMs)",
                 "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                "traffic": None, "launches_per_forward": len(gemm),
+                "traffic": measured_traffic(), "launches_per_forward": len(gemm),
                 "avg_launch_ms": round(g_avg_ms, 5),
                 "flops_per_launch_avg": g_flops / len(gemm)}
     breakdown = {k: {"launches": v[0], "ms": round(v[1], 4),
