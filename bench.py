@@ -31,6 +31,75 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
+def time_steps(m, ids_t, mask_t, out, steps, warmup):
+    import torch
+    for _ in range(warmup):
+        m.forward(ids_t, mask_t, out)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        m.forward(ids_t, mask_t, out)
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) * 1e3 / steps
+
+
+def cold_call(m, ids_t, mask_t):
+    """First forward on a new (batch, sequence, buffers) key in a warm process:
+    capture + instantiate + run of its graph(s)."""
+    import torch
+    out = m.new_logits(*ids_t.shape)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    m.forward(ids_t, mask_t, out)
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) * 1e3, out
+
+
+def fragmented(m, ids_t, mask_t, args):
+    """The same forward run as the unmended program (one graph per region
+    between graph breaks; host sync + read-back + host branch at each break)
+    next to the single-graph forward, both measured the same way (wall clock
+    around the loop, synchronised at both ends)."""
+    cold_g, out = cold_call(m, ids_t, mask_t)
+    ms_g = time_steps(m, ids_t, mask_t, out, args.steps, args.warmup)
+    m.set_exec_mode("fragmented")
+    s0 = m.stats()
+    cold_f, out = cold_call(m, ids_t, mask_t)
+    s1 = m.stats()
+    ms_f = time_steps(m, ids_t, mask_t, out, args.steps, args.warmup)
+    s2 = m.stats()
+    m.set_exec_mode("graph")
+    runs = args.steps + args.warmup
+    return {"single_graph": {"ms_per_step": round(ms_g, 4), "cold_ms": round(cold_g, 2)},
+            "fragmented": {"ms_per_step": round(ms_f, 4), "cold_ms": round(cold_f, 2),
+                           "graphs_per_forward": (s2["graph_launches"] - s1["graph_launches"]) / runs,
+                           "host_syncs_per_forward": (s2["host_syncs_in_forward"] - s1["host_syncs_in_forward"]) / runs,
+                           "graphs_captured": s1["captures"] - s0["captures"]},
+            "steady_speedup": round(ms_f / ms_g, 3), "cold_speedup": round(cold_f / cold_g, 3)}
+
+
+def break_suite(args):
+    """Single graph vs graph-broken forward on every workload (stderr)."""
+    import torch
+    import synth
+    from paper_2509_16248_amd.model import GmModel
+    for name in ["tiny_decoder", "causal_lm_768", "encoder_1024", "encoder_clamp_1024",
+                 "decoder_4096"]:
+        cfg = synth.preset(name)
+        w = synth.make_weights(cfg, 5)
+        ids, mask = synth.make_inputs(cfg, 0)
+        m = GmModel(cfg, w.globals, w.layers, device="cuda:0")
+        del w
+        ids_t = torch.from_numpy(ids).cuda()
+        mask_t = torch.from_numpy(mask).cuda()
+        cold_call(m, ids_t, mask_t)           # first capture of the process for this model
+        r = fragmented(m, ids_t, mask_t, args)
+        r["tokens"] = int(ids.size)
+        log("[breaks] " + json.dumps({name: r}))
+        m.close()
+        torch.cuda.empty_cache()
+
+
 def measured_traffic():
     """HBM bytes per GEMM launch from the committed rocprofv3 FETCH_SIZE /
     WRITE_SIZE summary, if it was taken on the GEMM source as it is now."""
@@ -71,6 +140,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=2)
+    ap.add_argument("--no-fragmented", action="store_true",
+                    help="skip the graph-broken baseline (same kernels, host sync per break)")
+    ap.add_argument("--break-suite", action="store_true",
+                    help="only compare single-graph and graph-broken forwards on every workload")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU (got --gpus {args.gpus}); "
@@ -83,6 +156,9 @@ def main():
     import synth
     from paper_2509_16248_amd.model import GmModel
 
+    if args.break_suite:
+        break_suite(args)
+        return
     cfg = synth.preset(WORKLOAD)
     B, S = cfg.batch, cfg.seq
     log(f"[bench] generating weights for {WORKLOAD}")
@@ -174,6 +250,9 @@ def main():
         "roofline": roofline,
         "kernel_breakdown_eager_ms": breakdown,
     }
+    if not args.no_fragmented:
+        result["fragmented_baseline"] = fragmented(m, ids_t, mask_t, args)
+        log(f"[bench] single graph vs graph-broken: {result['fragmented_baseline']}")
     m.close()
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a sample")

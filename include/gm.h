@@ -46,6 +46,7 @@ extern "C" {
 #define GM_E_NOMEM    -2  /* device allocation failed (gm_model_create only)  */
 #define GM_E_HIP      -3  /* a HIP runtime call failed; see gm_last_error     */
 #define GM_E_CAPTURE  -4  /* graph capture or instantiation failed            */
+#define GM_E_TRAP     -5  /* fragmented execution only: an input guard failed */
 
 /* ------------------------------------------------------------ enums */
 enum { GM_DTYPE_F32 = 0, GM_DTYPE_BF16 = 1, GM_DTYPE_F16 = 2 };
@@ -57,6 +58,9 @@ enum { GM_POS_NONE = 0, GM_POS_LEARNED = 1, GM_POS_ROTARY = 2 };
 /* Trap codes, in the order the guards run (smaller code = earlier guard). */
 enum { GM_TRAP_NONE = 0, GM_TRAP_TOKEN_RANGE = 1, GM_TRAP_MASK_VALUE = 2,
        GM_TRAP_ROPE_CAPACITY = 3 };
+
+/* Execution modes (gm_set_exec_mode). */
+enum { GM_EXEC_GRAPH = 0, GM_EXEC_EAGER = 1, GM_EXEC_FRAGMENTED = 2 };
 
 /* Kinds of deferred effect records (rule [Defer]). */
 enum { GM_EFFECT_PAD = 1, GM_EFFECT_REGROW = 2, GM_EFFECT_CLAMP = 3 };
@@ -204,8 +208,20 @@ int gm_profile_forward(gm_model *m, int32_t B, int32_t S, const int32_t *token_i
                        const int32_t *attn_mask, void *out_logits, hipStream_t stream,
                        gm_kernel_time *out, int32_t cap, int32_t *n_out);
 
-/* Use one captured hipGraph per forward (enabled = 1, the default) or
- * enqueue the kernels one by one (enabled = 0; same kernels, same results). */
+/* How gm_forward runs the same kernels (same results in every mode):
+ *  GM_EXEC_GRAPH (default)  one captured hipGraph per forward, no host sync;
+ *  GM_EXEC_EAGER            kernels enqueued one by one, no host sync;
+ *  GM_EXEC_FRAGMENTED       the unmended program the paper starts from: one
+ *    captured graph per region between graph breaks, and at every break a
+ *    hipStreamSynchronize, a device-to-host copy of the predicate's inputs
+ *    and the branch evaluated on the host (after the input guards / padding
+ *    / rotary predicates, and after every fp16 clamp site).  A failed guard
+ *    ends the forward there and returns GM_E_TRAP (the original `raise`).
+ *    Synchronous; for comparisons only (Evaluation, "Overhead Analysis of
+ *    Graph Breaks": sync + D2H copy + host evaluation per break). */
+int gm_set_exec_mode(gm_model *m, int32_t mode);
+
+/* gm_set_exec_mode(m, enabled ? GM_EXEC_GRAPH : GM_EXEC_EAGER). */
 int gm_set_graph_mode(gm_model *m, int32_t enabled);
 
 /* Copy the decisions of the last forward enqueued on `stream` into *out.

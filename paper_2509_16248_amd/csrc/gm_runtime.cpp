@@ -77,7 +77,15 @@ struct gm_model {
   hipStream_t cap_stream = nullptr;
   std::vector<GraphEntry> graphs;
   gm_stats stats;
-  bool graph_mode = true;
+  int exec_mode = GM_EXEC_GRAPH;
+  bool last_host_pad_any = false, last_host_regrow = false, last_host_clamp = false;
+  struct Frag {
+    int B, S;
+    const void *ids, *mask;
+    void* logits;
+    std::vector<hipGraphExec_t> execs;
+  };
+  std::vector<Frag> frags;
   bool debug_sync = false;
   uint64_t tick = 0;
 
@@ -229,9 +237,23 @@ struct Prof {
   }
 };
 
+// Segment selection for the fragmented (unmended) execution: the forward is
+// cut at every point where the original program reads a device value back
+// on the host; only the launches of segment `want` are issued (want < 0:
+// all, want == kCountOnly: none, just count the cuts).
+struct Seg {
+  int want = -1;
+  int cur = 0;
+};
+constexpr int kCountOnly = -2;
+
 void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
-             void* logits, hipStream_t s, Prof* prof = nullptr) {
+             void* logits, hipStream_t s, Prof* prof = nullptr, Seg* seg = nullptr) {
   const gm_config& c = m->cfg;
+  auto on = [&]() { return !seg || seg->want == -1 || seg->want == seg->cur; };
+  auto brk = [&]() {
+    if (seg) ++seg->cur;
+  };
   const int T = B * S, d = c.d_model, hd = d / c.n_heads, ff = c.d_ff;
   const int ns = n_sites(c);
   const float thr = 65504.f - c.clamp_margin;
@@ -244,11 +266,13 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
     if (prof) prof->mark(kind, layer, flops, bytes);
   };
   if (prof) prof->start();
-  launch_prologue(ids, mask, B, S, c.vocab, c.pos == GM_POS_ROTARY, c.rope_capacity, ns,
-                  m->state, s);
+  if (on())
+    launch_prologue(ids, mask, B, S, c.vocab, c.pos == GM_POS_ROTARY, c.rope_capacity, ns,
+                    m->state, s);
   P(GM_K_PROLOGUE, -1, 0.0, 8.0 * T);
+  brk();  // original program: guards, mask.any() and max(position_ids) read on the host
   if (c.pos == GM_POS_ROTARY) {
-    launch_rope_fill(m->rope_cos, m->rope_sin, hd, c.rope_base, m->state, s);
+    if (on()) launch_rope_fill(m->rope_cos, m->rope_sin, hd, c.rope_base, m->state, s);
     P(GM_K_ROPE, -1, 0.0, 0.0);
   }
 
@@ -271,7 +295,7 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
   r.b = m->emb_ln_b;
   r.out = m->h;
   r.clamp_site = -1;
-  launch_rownorm(r, s);
+  if (on()) launch_rownorm(r, s);
   P(GM_K_EMBED, -1, 0.0, static_cast<double>(T) * d * es * (c.pos == GM_POS_LEARNED ? 3 : 2));
   r.ids = nullptr;
 
@@ -283,7 +307,7 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
     q.g = g;
     q.b = b;
     q.clamp_site = site;
-    launch_rownorm(q, s);
+    if (on()) launch_rownorm(q, s);
     P(GM_K_NORM, cur_layer, 0.0, 2.0 * T * d * es);
   };
 
@@ -314,11 +338,12 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
     q.resid = resid;
     q.ldr = ldo;
     q.site = site;
-    launch_gemm(q, s);
+    if (on()) launch_gemm(q, s);
     const int nout = (epi == kEpiGatedGelu || epi == kEpiGatedSilu) ? N / 2 : N;
     P(kind, cur_layer, 2.0 * T * static_cast<double>(N) * K,
       es * (static_cast<double>(T) * K + static_cast<double>(N) * K +
             static_cast<double>(T) * nout * (resid ? 2 : 1)));
+    if (site >= 0) brk();  // original program: abs(h).max() read on the host
   };
 
   AttnArgs at{};
@@ -343,7 +368,7 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
   const double attn_flops = 4.0 * hd * pairs * B * c.n_heads;
   const double attn_bytes = es * (static_cast<double>(T) * 3 * d + static_cast<double>(T) * d);
   auto attention = [&]() {
-    launch_attention(at, s);
+    if (on()) launch_attention(at, s);
     P(GM_K_ATTENTION, cur_layer, attn_flops, attn_bytes);
   };
   int prev_site = -1;
@@ -377,7 +402,7 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
     z = m->a;
   }
   gemm(GM_K_GEMM_HEAD, z, d, m->head, c.vocab, kEpiStore, nullptr, logits, c.vocab, nullptr, -1);
-  launch_emit_effects(m->state, m->fifo, kFifoCap, ns, s);
+  if (on()) launch_emit_effects(m->state, m->fifo, kFifoCap, ns, s);
   P(GM_K_EFFECTS, -1, 0.0, 0.0);
 }
 
@@ -392,6 +417,7 @@ const char* gm_strerror(int code) {
     case GM_E_NOMEM: return "out of device memory";
     case GM_E_HIP: return "HIP runtime error";
     case GM_E_CAPTURE: return "graph capture failed";
+    case GM_E_TRAP: return "input guard failed";
     default: return "unknown error";
   }
 }
@@ -402,6 +428,8 @@ void gm_model_destroy(gm_model* m) {
   if (!m) return;
   hipDeviceSynchronize();
   for (auto& g : m->graphs) hipGraphExecDestroy(g.exec);
+  for (auto& f : m->frags)
+    for (hipGraphExec_t e : f.execs) hipGraphExecDestroy(e);
   if (m->cap_stream) hipStreamDestroy(m->cap_stream);
   for (void* p : m->allocs) hipFree(p);
   delete m;
@@ -544,9 +572,96 @@ int gm_model_create(const gm_config* cfg, const gm_weights* w, gm_model** out) {
   return GM_OK;
 }
 
-int gm_set_graph_mode(gm_model* m, int32_t enabled) {
+int gm_set_exec_mode(gm_model* m, int32_t mode) {
   if (!m) return inval("model is NULL");
-  m->graph_mode = enabled != 0;
+  if (mode != GM_EXEC_GRAPH && mode != GM_EXEC_EAGER && mode != GM_EXEC_FRAGMENTED)
+    return inval("bad execution mode");
+  m->exec_mode = mode;
+  return GM_OK;
+}
+
+int gm_set_graph_mode(gm_model* m, int32_t enabled) {
+  return gm_set_exec_mode(m, enabled ? GM_EXEC_GRAPH : GM_EXEC_EAGER);
+}
+
+// The unmended program: every data-dependent branch is a host decision.  Each
+// stretch between two such reads is one captured graph (one per fused
+// region, as the paper's baseline captures them); at each cut the host
+// synchronises the stream, copies the predicate's inputs back and evaluates
+// the branch.  The kernels are the same as in the single-graph forward.
+static int forward_fragmented(gm_model* m, int B, int S, const int32_t* ids,
+                              const int32_t* mask, void* logits, hipStream_t stream) {
+  gm_model::Frag* fr = nullptr;
+  for (auto& f : m->frags)
+    if (f.B == B && f.S == S && f.ids == ids && f.mask == mask && f.logits == logits) fr = &f;
+  if (!fr) {
+    Seg count;
+    count.want = kCountOnly;
+    enqueue(m, B, S, ids, mask, logits, m->cap_stream, nullptr, &count);
+    gm_model::Frag f{B, S, ids, mask, logits, {}};
+    for (int i = 0; i <= count.cur; ++i) {
+      hipGraph_t graph = nullptr;
+      HIP_TRY(hipStreamBeginCapture(m->cap_stream, hipStreamCaptureModeThreadLocal));
+      Seg sg;
+      sg.want = i;
+      enqueue(m, B, S, ids, mask, logits, m->cap_stream, nullptr, &sg);
+      hipError_t e = hipStreamEndCapture(m->cap_stream, &graph);
+      if (e != hipSuccess || !graph) {
+        g_last_error = std::string("capture: ") + hipGetErrorString(e);
+        return GM_E_CAPTURE;
+      }
+      hipGraphExec_t exec = nullptr;
+      e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+      hipGraphDestroy(graph);
+      if (e != hipSuccess) {
+        g_last_error = std::string("instantiate: ") + hipGetErrorString(e);
+        return GM_E_CAPTURE;
+      }
+      f.execs.push_back(exec);
+      m->stats.captures++;
+    }
+    m->frags.push_back(std::move(f));
+    fr = &m->frags.back();
+  }
+  const gm_config& c = m->cfg;
+  const int ns = n_sites(c);
+  const float thr = 65504.f - c.clamp_margin;
+  const int nseg = static_cast<int>(fr->execs.size());
+  int32_t host[kAbsmaxBase + 2 * GM_MAX_LAYERS];
+  for (int i = 0; i < nseg; ++i) {
+    HIP_TRY(hipGraphLaunch(fr->execs[i], stream));
+    m->stats.graph_launches++;
+    if (i + 1 == nseg) break;
+    // graph break: wait for the device, read the predicate back, branch on the host
+    m->stats.host_syncs_in_forward++;
+    HIP_TRY(hipStreamSynchronize(stream));
+    if (i == 0) {
+      HIP_TRY(hipMemcpy(host, m->state, sizeof(int32_t) * kClampBase, hipMemcpyDeviceToHost));
+      const uint32_t trap = static_cast<uint32_t>(host[kTrapFwd]);
+      if (trap != kTrapNone) {  // `if not C: raise` -- the forward stops at the guard
+        int32_t sticky = 0;
+        HIP_TRY(hipMemcpy(&sticky, m->state + kTrapSticky, sizeof(sticky), hipMemcpyDeviceToHost));
+        if (!sticky) {
+          sticky = static_cast<int32_t>(trap);
+          HIP_TRY(hipMemcpy(m->state + kTrapSticky, &sticky, sizeof(sticky), hipMemcpyHostToDevice));
+        }
+        g_last_error = "input guard failed (fragmented execution stops at the guard)";
+        return GM_E_TRAP;
+      }
+      m->last_host_pad_any = host[kPadAny] != 0;      // `if mask.any():`
+      m->last_host_regrow = host[kRegrow] != 0;       // `if seq_len > cached:`
+    } else {
+      const int site = i - 1;
+      if (site < ns) {
+        int32_t am[2];
+        HIP_TRY(hipMemcpy(&am[0], m->state + kAbsmaxBase + site, sizeof(int32_t), hipMemcpyDeviceToHost));
+        HIP_TRY(hipMemcpy(&am[1], m->state + kNanBase + site, sizeof(int32_t), hipMemcpyDeviceToHost));
+        float mx;
+        memcpy(&mx, &am[0], sizeof(mx));
+        m->last_host_clamp = !am[1] && mx > thr;      // `if abs(h).max() > thr:`
+      }
+    }
+  }
   return GM_OK;
 }
 
@@ -557,7 +672,8 @@ int gm_forward_ex(gm_model* m, int32_t B, int32_t S, const int32_t* ids, const i
   if (B < 1 || B > m->cfg.max_batch || S < 1 || S > m->cfg.max_seq)
     return inval("B or S out of range");
   m->stats.forwards++;
-  if (!m->graph_mode) {
+  if (m->exec_mode == GM_EXEC_FRAGMENTED) return forward_fragmented(m, B, S, ids, mask, logits, stream);
+  if (m->exec_mode == GM_EXEC_EAGER) {
     enqueue(m, B, S, ids, mask, logits, stream);
     HIP_TRY(hipGetLastError());
     m->stats.eager_forwards++;

@@ -15,7 +15,8 @@ LIB_PATH = os.path.join(_HERE, "libgm.so")
 
 GM_ABI_VERSION = 1
 GM_MAX_LAYERS = 64
-GM_OK, GM_E_INVAL, GM_E_NOMEM, GM_E_HIP, GM_E_CAPTURE = 0, -1, -2, -3, -4
+GM_OK, GM_E_INVAL, GM_E_NOMEM, GM_E_HIP, GM_E_CAPTURE, GM_E_TRAP = 0, -1, -2, -3, -4, -5
+GM_EXEC_GRAPH, GM_EXEC_EAGER, GM_EXEC_FRAGMENTED = 0, 1, 2
 GM_DTYPE_F32, GM_DTYPE_BF16, GM_DTYPE_F16 = 0, 1, 2
 GM_NORM_LAYER, GM_NORM_RMS = 0, 1
 GM_NORM_PRE, GM_NORM_POST = 0, 1
@@ -82,7 +83,7 @@ KERNEL_KINDS = ["prologue", "rope_fill", "embed", "norm", "gemm_qkv", "attention
 gm_effect_cb = ctypes.CFUNCTYPE(None, ctypes.POINTER(gm_effect), ctypes.c_void_p)
 
 EXPORTS = ["gm_model_create", "gm_model_destroy", "gm_forward", "gm_forward_ex",
-           "gm_profile_forward", "gm_set_graph_mode", "gm_read_decisions", "gm_decisions_device_ptr",
+           "gm_profile_forward", "gm_set_exec_mode", "gm_set_graph_mode", "gm_read_decisions", "gm_decisions_device_ptr",
            "gm_check_error", "gm_flush_effects", "gm_debug_buffer", "gm_get_stats",
            "gm_strerror",
            "gm_last_error"]
@@ -106,6 +107,7 @@ def lib(path: str = LIB_PATH) -> ctypes.CDLL:
     L.gm_forward.argtypes = [_vp, _vp, _vp, _vp, _vp]
     L.gm_forward_ex.argtypes = [_vp, _i32, _i32, _vp, _vp, _vp, _vp]
     L.gm_set_graph_mode.argtypes = [_vp, _i32]
+    L.gm_set_exec_mode.argtypes = [_vp, _i32]
     L.gm_profile_forward.argtypes = [_vp, _i32, _i32, _vp, _vp, _vp, _vp,
                                      ctypes.POINTER(gm_kernel_time), _i32, ctypes.POINTER(_i32)]
     L.gm_read_decisions.argtypes = [_vp, ctypes.POINTER(gm_decisions), _vp]
@@ -170,6 +172,10 @@ def gm_profile_forward(m: int, B: int, S: int, ids: int, mask: int, logits: int,
                                     ctypes.byref(n)), "gm_profile_forward")
     return [(KERNEL_KINDS[arr[i].kind], arr[i].layer, arr[i].ms, arr[i].flops, arr[i].bytes)
             for i in range(min(n.value, cap))]
+
+
+def gm_set_exec_mode(m: int, mode: int) -> None:
+    _check(lib().gm_set_exec_mode(m, int(mode)), "gm_set_exec_mode")
 
 
 def gm_set_graph_mode(m: int, enabled: bool) -> None:

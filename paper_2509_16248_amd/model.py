@@ -111,6 +111,12 @@ class GmModel:
     def set_graph_mode(self, enabled: bool):
         gm.gm_set_graph_mode(self.handle, enabled)
 
+    def set_exec_mode(self, mode: str):
+        """'graph' (default), 'eager' or 'fragmented' (the unmended program:
+        one graph per region, host sync + read-back at every graph break)."""
+        gm.gm_set_exec_mode(self.handle, {"graph": gm.GM_EXEC_GRAPH, "eager": gm.GM_EXEC_EAGER,
+                                          "fragmented": gm.GM_EXEC_FRAGMENTED}[mode])
+
     def decisions(self, stream=None) -> dict:
         d = gm.gm_read_decisions(self.handle, self._stream(stream))
         n = d.n_clamp_sites
