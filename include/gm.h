@@ -185,6 +185,8 @@ void gm_model_destroy(gm_model *m);
  *  token_ids  device int32 [B, S] row-major, each in [0, vocab)
  *  attn_mask  device int32 [B, S] row-major, 1 = token, 0 = padding
  *  out_logits device [B, S, vocab] in act_dtype, row-major
+ * All three pointers must be 16-byte aligned (GM_E_INVAL otherwise; every
+ * allocator in use returns at least that).
  * Asynchronous: no host synchronisation, no device-to-host copy and no
  * allocation once the (B, S, pointers) combination has been seen; the first
  * call with a new combination captures and instantiates a graph (cold

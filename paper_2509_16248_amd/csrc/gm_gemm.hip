@@ -3,7 +3,7 @@
 // A is [M, K] (activations, row-major), W is [N, K] (nn.Linear weight
 // layout, row-major): both operands are contiguous along K, which is the
 // operand layout the matrix cores read.  bf16/fp16 run on gfx950 MFMA
-// (v_mfma_f32_16x16x32_{bf16,f16}) with fp32 accumulation; fp32 runs on a
+// (v_mfma_f32_32x32x16_{bf16,f16}) with fp32 accumulation; fp32 runs on a
 // plain LDS-tiled FMA kernel.  All epilogues work on fp32 accumulators and
 // round once to the storage dtype.
 #include <math.h>
@@ -19,20 +19,6 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
-
-template <typename T> struct Mfma;
-template <> struct Mfma<bf16_t> {
-  typedef bf16x8 vec;
-  static __device__ __forceinline__ f32x4 run(vec a, vec b, f32x4 c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-  }
-};
-template <> struct Mfma<f16_t> {
-  typedef f16x8 vec;
-  static __device__ __forceinline__ f32x4 run(vec a, vec b, f32x4 c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
-  }
-};
 
 // ------------------------------------------------------------ epilogue
 template <typename T>
@@ -185,108 +171,9 @@ __device__ __forceinline__ void site_flush(const GemmArgs& a, SiteMax& sm) {
   }
 }
 
-// ------------------------------------------------------------ MFMA kernel
-// Workgroup tile 128 x 128, K step 64, 4 wavefronts in a 2 x 2 grid, each
-// wavefront 64 x 64 = 4 x 4 MFMA tiles of 16 x 16.  W is the MFMA A operand
-// and A the B operand, so each lane ends up with 4 consecutive output
-// columns of one row (vector stores, pair epilogues in registers).
-// Operand tiles are staged in LDS with a 16-byte row pad; the next K step is
-// prefetched into registers while the current one is multiplied.
-constexpr int kBM = 128, kBN = 128, kBK = 64, kLDK = kBK + 8;
-
-template <typename T>
-__global__ __launch_bounds__(256) void k_gemm_mfma(GemmArgs a) {
-  typedef typename Mfma<T>::vec vec;
-  __shared__ __attribute__((aligned(16))) T sA[2][kBM * kLDK];
-  __shared__ __attribute__((aligned(16))) T sB[2][kBN * kLDK];
-  const int tiles_n = (a.N + kBN - 1) / kBN;
-  const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
-  const int bm = tm * kBM, bn = tn * kBN;
-  const int t = threadIdx.x;
-  const int lrow = t >> 3, lcol = (t & 7) * 8;
-  const T* Ag[4];
-  const T* Wg[4];
-#pragma unroll
-  for (int v = 0; v < 4; ++v) {
-    int r = bm + lrow + 32 * v;
-    r = r < a.M ? r : a.M - 1;
-    Ag[v] = static_cast<const T*>(a.A) + static_cast<long long>(r) * a.lda + lcol;
-    int c = bn + lrow + 32 * v;
-    c = c < a.N ? c : a.N - 1;
-    Wg[v] = static_cast<const T*>(a.W) + static_cast<long long>(c) * a.ldw + lcol;
-  }
-  u32x4 ra[4], rb[4];
-  auto gload = [&](int k0) {
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      ra[v] = *reinterpret_cast<const u32x4*>(Ag[v] + k0);
-      rb[v] = *reinterpret_cast<const u32x4*>(Wg[v] + k0);
-    }
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      *reinterpret_cast<u32x4*>(&sA[buf][(lrow + 32 * v) * kLDK + lcol]) = ra[v];
-      *reinterpret_cast<u32x4*>(&sB[buf][(lrow + 32 * v) * kLDK + lcol]) = rb[v];
-    }
-  };
-  const int wave = t >> 6, lane = t & 63;
-  const int wm = wave >> 1, wn = wave & 1;
-  const int l16 = lane & 15, g = lane >> 4;
-  f32x4 acc[4][4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  const int nk = a.K / kBK;
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) gload((kt + 1) * kBK);
-#pragma unroll
-    for (int kc = 0; kc < 2; ++kc) {
-      vec af[4], bfr[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        af[i] = *reinterpret_cast<const vec*>(
-            &sA[buf][(wm * 64 + 16 * i + l16) * kLDK + kc * 32 + g * 8]);
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        bfr[j] = *reinterpret_cast<const vec*>(
-            &sB[buf][(wn * 64 + 16 * j + l16) * kLDK + kc * 32 + g * 8]);
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = Mfma<T>::run(bfr[j], af[i], acc[i][j]);
-    }
-    if (kt + 1 < nk) sstore(buf ^ 1);
-    __syncthreads();
-  }
-
-  SiteMax sm;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int m = bm + wm * 64 + 16 * i + l16;
-#pragma unroll
-    for (int j = 0; j < 4; j += 2) {
-      const int nA = bn + wn * 64 + 16 * j + 4 * g;
-      float va[4], vb[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        va[r] = acc[i][j][r];
-        vb[r] = acc[i][j + 1][r];
-      }
-      epi_pair<T>(a, m, nA, va, vb, sm);
-    }
-  }
-  site_flush(a, sm);
-}
-
-
 // ------------------------------------------------------------ MFMA 32x32 kernel
+constexpr int kBK = 64, kLDK = kBK + 8;   // K step; padded LDS row (elements)
+
 // Workgroup tile BM x BN (256 x 256 or 128 x 128), K step 64, 4 wavefronts
 // in a 2 x 2 grid; each wavefront owns (BM/2) x (BN/2) as TM x TN tiles of
 // v_mfma_f32_32x32x16 (bf16/f16 in, fp32 accumulate).  W is the MFMA A
@@ -443,23 +330,25 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm_x(GemmArgs a) {
   // register set (stage % PF).  At the end of iteration k, set (k+1) % PF
   // (fetched PF-1 iterations earlier) goes to the other LDS buffer.  The loop
   // is unrolled by PF so every set index is a compile-time constant.
-  static_for<0, PF>([&](auto st) {
-    if (st < nk) gload(st, st * kBK);
-  });
+  // Every iteration issues its loads unconditionally (stages past the end
+  // re-read the last one): the number of loads in flight is then the same on
+  // every path, and the wait before an LDS store lets the younger PF - 1
+  // stages stay in flight instead of draining all of them.
+  auto stage = [&](int k) { return (k < nk ? k : nk - 1) * kBK; };
+  static_for<0, PF>([&](auto st) { gload(st, stage(st)); });
   sstore(std::integral_constant<int, 0>{}, 0);
   __syncthreads();
-  auto iter = [&](auto P, int k) {
-    constexpr int p = decltype(P)::value;          // k % PF
-    constexpr int nxt = (p + 1) % PF;              // set holding stage k + 1
-    if (PF > 1 && k + PF < nk) gload(P, (k + PF) * kBK);   // set p is free again
-    if (PF == 1 && k + 1 < nk) gload(P, (k + 1) * kBK);
-    compute(k & 1);
-    if (k + 1 < nk) sstore(std::integral_constant<int, nxt>{}, (k + 1) & 1);
-    __syncthreads();
-  };
   for (int kt = 0; kt < nk; kt += PF) {
     static_for<0, PF>([&](auto P) {
-      if (kt + P < nk) iter(P, kt + P);
+      constexpr int p = decltype(P)::value;        // k % PF
+      constexpr int nxt = (p + 1) % PF;            // set holding stage k + 1
+      const int k = kt + p;
+      gload(P, stage(k + PF));                     // set p went to LDS last iteration
+      if (k < nk) {
+        compute(k & 1);
+        if (k + 1 < nk) sstore(std::integral_constant<int, nxt>{}, (k + 1) & 1);
+        __syncthreads();
+      }
     });
   }
 
@@ -467,11 +356,15 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm_x(GemmArgs a) {
   if (STAGE && (a.epi == kEpiStore || a.epi == kEpiGelu || a.epi == kEpiResid)) {
     // Column-independent epilogues go through LDS: bias (and GELU) are
     // applied in registers, the fp32 tile is staged, and rows are then
-    // written with consecutive lanes on consecutive columns, so the stores
-    // coalesce whatever the alignment of the output rows (the vocabulary
-    // of the head may be odd).
+    // written by consecutive lanes on consecutive columns: 16-byte chunks
+    // when output (and residual) rows are 16-byte aligned, single elements
+    // otherwise (the odd vocabulary of the head).
     float* st = reinterpret_cast<float*>(smem);
     const T* bias = static_cast<const T*>(a.bias);
+    T* out = static_cast<T*>(a.out);
+    const T* res = static_cast<const T*>(a.resid);
+    const bool resid = a.epi == kEpiResid;
+    const bool aligned = (a.ldo & 7) == 0 && (!resid || (a.ldr & 7) == 0);
     static_for<0, TM>([&](auto i) {
       const int ml = wm * WTM + 32 * i + l32;
       static_for<0, TN>([&](auto j) {
@@ -490,41 +383,53 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm_x(GemmArgs a) {
       });
     });
     __syncthreads();
-    T* out = static_cast<T*>(a.out);
-    const T* res = static_cast<const T*>(a.resid);
-    const bool resid = a.epi == kEpiResid;
-    if ((a.ldo & 7) == 0 && (!resid || (a.ldr & 7) == 0) && bn + BN <= a.N) {
-      // 16-byte stores: a row is BN/8 chunks
+    if (aligned) {
       constexpr int CPR = BN / 8;
+      const int ncol = a.N - bn < BN ? a.N - bn : BN;
       for (int e = t; e < BM * CPR; e += NT) {
-        const int ml = e / CPR, c = (e % CPR) * 8;
+        const int ml = e / CPR, k = e % CPR;
         const int m = bm + ml;
-        if (m >= a.M) continue;
+        const int j0 = 8 * k;
+        if (m >= a.M || j0 >= ncol) continue;
+        const f32x4v lo = *reinterpret_cast<const f32x4v*>(&st[ml * LDC + 8 * k]);
+        const f32x4v hi = *reinterpret_cast<const f32x4v*>(&st[ml * LDC + 8 * k + 4]);
         float v[8];
-        const f32x4v lo = *reinterpret_cast<const f32x4v*>(&st[ml * LDC + c]);
-        const f32x4v hi = *reinterpret_cast<const f32x4v*>(&st[ml * LDC + c + 4]);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           v[r] = lo[r];
           v[4 + r] = hi[r];
         }
-        if (resid) {
-          const u32x4 rr = *reinterpret_cast<const u32x4*>(res + static_cast<long long>(m) * a.ldr + bn + c);
-          const T* re = reinterpret_cast<const T*>(&rr);
+        T* orow = out + static_cast<long long>(m) * a.ldo + bn;
+        if (j0 + 8 <= ncol) {
+          if (resid) {
+            const u32x4 rr = *reinterpret_cast<const u32x4*>(res + static_cast<long long>(m) * a.ldr + bn + j0);
+            const T* re = reinterpret_cast<const T*>(&rr);
 #pragma unroll
-          for (int r = 0; r < 8; ++r) v[r] += to_f32(re[r]);
-        }
-        u32x4 w;
-        T* we = reinterpret_cast<T*>(&w);
+            for (int r = 0; r < 8; ++r) v[r] += to_f32(re[r]);
+          }
+          u32x4 w;
+          T* we = reinterpret_cast<T*>(&w);
 #pragma unroll
-        for (int r = 0; r < 8; ++r) {
-          we[r] = from_f32<T>(v[r]);
-          if (resid && a.site >= 0) sm.add(to_f32(we[r]));
+          for (int r = 0; r < 8; ++r) {
+            we[r] = from_f32<T>(v[r]);
+            if (resid && a.site >= 0) sm.add(to_f32(we[r]));
+          }
+          *reinterpret_cast<u32x4*>(orow + j0) = w;
+        } else {
+          // last chunk of a partial tile
+#pragma unroll
+          for (int r = 0; r < 8; ++r) {
+            const int jj = j0 + r;
+            if (jj >= ncol) continue;
+            float y = v[r];
+            if (resid) y += to_f32(res[static_cast<long long>(m) * a.ldr + bn + jj]);
+            const T o = from_f32<T>(y);
+            if (resid && a.site >= 0) sm.add(to_f32(o));
+            orow[jj] = o;
+          }
         }
-        *reinterpret_cast<u32x4*>(out + static_cast<long long>(m) * a.ldo + bn + c) = w;
       }
     } else {
-      // element stores, consecutive lanes on consecutive columns
       for (int e = t; e < BM * BN; e += NT) {
         const int ml = e / BN, nl = e % BN;
         const int m = bm + ml, n = bn + nl;
@@ -563,8 +468,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm_x(GemmArgs a) {
 // one is multiplied.  One wavefront instruction fills 1 KB of LDS, lane i at
 // byte 16*i, i.e. 8 tile rows of 128 bytes; the lane chooses which 16-byte
 // chunk of its row it fetches so that row r's chunk c lands in slot
-// c ^ (r & 7) (XOR swizzle: the 32 rows an MFMA operand read touches hit
-// distinct banks).  Waits are explicit (s_waitcnt vmcnt + s_barrier); the
+// c ^ ((r >> 1) & 7).  LDS serves a 16-byte read for 16 lanes at a time
+// from 64 four-byte banks (256 bytes, two tile rows): with this swizzle the
+// 16 consecutive rows an MFMA operand read touches at a time fall on 16
+// distinct 16-byte bank groups.  Waits are explicit (s_waitcnt vmcnt + s_barrier); the
 // compiler does not track the DMA writes.
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
@@ -609,7 +516,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm_dma(GemmArgs a) {
 #pragma unroll
   for (int j = 0; j < LPS; ++j) {
     const int sr = (wave * LPS + j) * 8 + (lane >> 3);
-    const int chunk = (lane & 7) ^ (sr & 7);
+    const int chunk = (lane & 7) ^ ((sr >> 1) & 7);
     if (sr < BM) {
       int r = bm + sr;
       r = r < a.M ? r : a.M - 1;
@@ -638,28 +545,42 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm_dma(GemmArgs a) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
+  // Fragment reads: row r's 16-byte chunk c sits in slot c ^ ((r >> 1) & 7);
+  // (r >> 1) & 7 only depends on the lane (rows differ by multiples of 32).
+  const int swz = (l32 >> 1) & 7;
+  const int offA = (wm * WTM + l32) * kBK, offB = BM * kBK + (wn * WTN + l32) * kBK;
+  vec fa[2][TM], fb[2][TN];
+  auto read_frags = [&](auto set, const T* st, int ks) {
+    const int col = ((2 * ks + g) ^ swz) << 3;
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+      fb[set][j] = *reinterpret_cast<const vec*>(st + offB + 32 * j * kBK + col);
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+      fa[set][i] = *reinterpret_cast<const vec*>(st + offA + 32 * i * kBK + col);
+  };
+  // One stage: the fragments of k-step ks + 1 are read while the MFMAs of
+  // k-step ks run (the scheduler is told to alternate one MFMA with one LDS
+  // read), so LDS latency hides behind matrix work.
   auto compute = [&](int stage_buf) {
-    const T* sa = lds + stage_buf * STAGE_ELEMS;
-    const T* sb = sa + BM * kBK;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const int c = 2 * ks + g;
-      vec af[TM], bfr[TN];
-#pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        const int r = wm * WTM + 32 * i + l32;
-        af[i] = *reinterpret_cast<const vec*>(sa + r * kBK + ((c ^ (r & 7)) << 3));
-      }
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int r = wn * WTN + 32 * j + l32;
-        bfr[j] = *reinterpret_cast<const vec*>(sb + r * kBK + ((c ^ (r & 7)) << 3));
-      }
+    const T* st = lds + stage_buf * STAGE_ELEMS;
+    read_frags(std::integral_constant<int, 0>{}, st, 0);
+    static_for<0, KS>([&](auto ks) {
+      constexpr int cur = decltype(ks)::value & 1;
+      if constexpr (decltype(ks)::value + 1 < KS)
+        read_frags(std::integral_constant<int, cur ^ 1>{}, st, decltype(ks)::value + 1);
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = Mfma32<T>::run(bfr[j], af[i], acc[i][j]);
-    }
+        for (int j = 0; j < TN; ++j) acc[i][j] = Mfma32<T>::run(fb[cur][j], fa[cur][i], acc[i][j]);
+      if constexpr (decltype(ks)::value + 1 < KS) {
+        static_for<0, TM * TN>([&](auto q) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);      // one MFMA
+          if constexpr (decltype(q)::value < TM + TN)
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);    // one LDS read
+        });
+      }
+    });
   };
 
   const int nk = a.K / kBK;
@@ -780,10 +701,12 @@ static void run_x(const GemmArgs& a, hipStream_t s) {
 
 template <typename T>
 static void gemm_mfma(const GemmArgs& a, hipStream_t s, int variant) {
+  // alternative configurations kept for measurement (GM_GEMM_VARIANT)
   switch (variant) {
-    case 6: run_x<T, 128, 128, 2, 2, 1>(a, s); return;
-    case 11: run_x<T, 128, 128, 2, 4, 1>(a, s); return;
+    case 12: run_x<T, 128, 128, 2, 4, 3>(a, s); return;
+    case 14: run_x<T, 128, 128, 2, 2, 2>(a, s); return;
     case 24: run_dma<T, 256, 256, 2, 4, 2>(a, s); return;
+    case 27: run_dma<T, 128, 128, 2, 4, 2>(a, s); return;
     default: break;
   }
   // 128 x 128 workgroup tiles, 8 wavefronts of 64 x 32, operands fetched two
@@ -848,12 +771,6 @@ void launch_gemm(const GemmArgs& a, hipStream_t s) {
     if (a.dtype == kF32) hipLaunchKernelGGL(k_gemm_simple<float>, grid, dim3(256), 0, s, a);
     else if (a.dtype == kBF16) hipLaunchKernelGGL(k_gemm_simple<bf16_t>, grid, dim3(256), 0, s, a);
     else hipLaunchKernelGGL(k_gemm_simple<f16_t>, grid, dim3(256), 0, s, a);
-    return;
-  }
-  if (g_gemm_variant == 1) {
-    const dim3 grid(((a.M + kBM - 1) / kBM) * ((a.N + kBN - 1) / kBN));
-    if (a.dtype == kBF16) hipLaunchKernelGGL(k_gemm_mfma<bf16_t>, grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL(k_gemm_mfma<f16_t>, grid, dim3(256), 0, s, a);
     return;
   }
   if (a.dtype == kBF16) gemm_mfma<bf16_t>(a, s, g_gemm_variant);

@@ -669,6 +669,9 @@ int gm_forward_ex(gm_model* m, int32_t B, int32_t S, const int32_t* ids, const i
                   void* logits, hipStream_t stream) {
   if (!m) return inval("model is NULL");
   if (!ids || !mask || !logits) return inval("ids, mask and logits must be non-NULL");
+  if ((reinterpret_cast<uintptr_t>(ids) | reinterpret_cast<uintptr_t>(mask) |
+       reinterpret_cast<uintptr_t>(logits)) & 15)
+    return inval("ids, mask and logits must be 16-byte aligned");
   if (B < 1 || B > m->cfg.max_batch || S < 1 || S > m->cfg.max_seq)
     return inval("B or S out of range");
   m->stats.forwards++;
@@ -732,6 +735,9 @@ int gm_profile_forward(gm_model* m, int32_t B, int32_t S, const int32_t* ids,
                        gm_kernel_time* out, int32_t cap, int32_t* n_out) {
   if (!m || !out || !n_out) return inval("NULL argument");
   if (!ids || !mask || !logits) return inval("ids, mask and logits must be non-NULL");
+  if ((reinterpret_cast<uintptr_t>(ids) | reinterpret_cast<uintptr_t>(mask) |
+       reinterpret_cast<uintptr_t>(logits)) & 15)
+    return inval("ids, mask and logits must be 16-byte aligned");
   if (B < 1 || B > m->cfg.max_batch || S < 1 || S > m->cfg.max_seq)
     return inval("B or S out of range");
   Prof prof;
