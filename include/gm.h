@@ -37,7 +37,7 @@
 extern "C" {
 #endif
 
-#define GM_ABI_VERSION 1
+#define GM_ABI_VERSION 2
 #define GM_MAX_LAYERS 64
 
 /* ------------------------------------------------------------ return codes */
@@ -57,7 +57,7 @@ enum { GM_POS_NONE = 0, GM_POS_LEARNED = 1, GM_POS_ROTARY = 2 };
 
 /* Trap codes, in the order the guards run (smaller code = earlier guard). */
 enum { GM_TRAP_NONE = 0, GM_TRAP_TOKEN_RANGE = 1, GM_TRAP_MASK_VALUE = 2,
-       GM_TRAP_ROPE_CAPACITY = 3 };
+       GM_TRAP_ROPE_CAPACITY = 3, GM_TRAP_KV_CAPACITY = 4 };
 
 /* Execution modes (gm_set_exec_mode). */
 enum { GM_EXEC_GRAPH = 0, GM_EXEC_EAGER = 1, GM_EXEC_FRAGMENTED = 2 };
@@ -79,6 +79,9 @@ enum { GM_EFFECT_PAD = 1, GM_EFFECT_REGROW = 2, GM_EFFECT_CLAMP = 3 };
  *  cached length) grows it on the device to exactly that length.
  *  fp16_clamp (f16 + PRE only): after each residual add, if no element is
  *  NaN and max |h| > 65504 - clamp_margin, h is clamped to that bound.
+ *  kv_cache (causal models without fp16_clamp): keep every layer's k and v
+ *  for max_batch x max_seq positions so that gm_decode_step can extend the
+ *  sequences of the last forward one token at a time.
  */
 typedef struct gm_config {
   int32_t abi_version;      /* must be GM_ABI_VERSION */
@@ -91,6 +94,7 @@ typedef struct gm_config {
   int32_t act_dtype;
   int32_t fp16_clamp;
   float   clamp_margin;
+  int32_t kv_cache;
 } gm_config;
 
 /* ------------------------------------------------------------ weights
@@ -145,7 +149,8 @@ typedef void (*gm_effect_cb)(const gm_effect *effect, void *user);
 /* Kernel kinds reported by gm_profile_forward. */
 enum { GM_K_PROLOGUE = 0, GM_K_ROPE = 1, GM_K_EMBED = 2, GM_K_NORM = 3,
        GM_K_GEMM_QKV = 4, GM_K_ATTENTION = 5, GM_K_GEMM_O = 6, GM_K_GEMM_UP = 7,
-       GM_K_GEMM_DOWN = 8, GM_K_GEMM_HEAD = 9, GM_K_EFFECTS = 10 };
+       GM_K_GEMM_DOWN = 8, GM_K_GEMM_HEAD = 9, GM_K_EFFECTS = 10, GM_K_KV_STORE = 11,
+       GM_K_ARGMAX = 12 };
 
 /* One kernel launch of a profiled forward.  flops/bytes are the launch's
  * algorithmic work (2*M*N*K for a GEMM; 4*hd*visible (query,key) pairs per
@@ -165,6 +170,7 @@ typedef struct gm_stats {
   uint64_t eager_forwards;   /* forwards enqueued without a graph             */
   uint64_t host_syncs_in_forward; /* sync-class HIP calls made inside a forward */
   uint64_t kernels_per_forward;   /* kernel nodes in the last captured graph  */
+  uint64_t decode_steps;     /* gm_decode_step calls                          */
 } gm_stats;
 
 /* ------------------------------------------------------------ entry points */
@@ -197,9 +203,34 @@ void gm_model_destroy(gm_model *m);
 int gm_forward(gm_model *m, const int32_t *token_ids, const int32_t *attn_mask,
                void *out_logits, hipStream_t stream);
 
-/* As gm_forward over B <= max_batch sequences of S <= max_seq tokens. */
+/* As gm_forward over B <= max_batch sequences of S <= max_seq tokens.  With
+ * kv_cache it also stores every position's k and v (with its mask value) and
+ * sets the length of sequence b to 1 + its last unmasked position: the
+ * prefill that gm_decode_step continues. */
 int gm_forward_ex(gm_model *m, int32_t B, int32_t S, const int32_t *token_ids,
                   const int32_t *attn_mask, void *out_logits, hipStream_t stream);
+
+/* One decode step (kv_cache models): append token_ids[b] to sequence b at
+ * position p_b = its current length, run the layer stack on those B rows
+ * with attention over the cached keys 0..p_b (keys the prefill masked stay
+ * masked), and write the logits of the new positions.  The result equals the
+ * last row of a full forward over the extended sequences (causal models:
+ * earlier positions do not depend on later ones).
+ *  B          must equal the batch of the last gm_forward_ex
+ *  token_ids  device int32 [B], each in [0, vocab)
+ *  out_logits device [B, vocab] in act_dtype
+ *  next_ids   device int32 [B] or NULL: greedy choice argmax_v logits[b, v]
+ *             (lowest index among equal values, the first NaN if any); may
+ *             equal token_ids, so that repeated steps generate greedily
+ *             without the host reading anything back
+ * All pointers 16-byte aligned.  Same asynchronous, one-graph-per-pointer-set
+ * behaviour as gm_forward.  Guards (trap word, smallest code first): token
+ * range (index b), rotary capacity, a sequence already at max_seq
+ * (GM_TRAP_KV_CAPACITY, index b); a trapped step stores nothing and leaves
+ * every length as it was.  The rotary regrow runs exactly as in a forward (need = max p_b + 1)
+ * and is recorded as a deferred effect.  Not available in fragmented mode. */
+int gm_decode_step(gm_model *m, int32_t B, const int32_t *token_ids, void *out_logits,
+                   int32_t *next_ids, hipStream_t stream);
 
 /* Run one forward without a graph, recording a HIP event on `stream` after
  * every kernel, wait for it, and write one gm_kernel_time per launch (in

@@ -15,8 +15,10 @@ parts and by a cross-check against PyTorch CPU functional operators.
 from .model import (EFFECT_CLAMP, EFFECT_PAD, EFFECT_REGROW, FP16_MAX,
                     TRAP_MASK_VALUE, TRAP_ROPE_CAPACITY, TRAP_TOKEN_RANGE,
                     Effect, OracleModel, OracleResult, Trap)
+from .decode import TRAP_KV_CAPACITY, DecodeStep, OracleDecoder, generate_greedy, greedy
 from . import numerics
 
 __all__ = ["OracleModel", "OracleResult", "Trap", "Effect", "numerics",
            "TRAP_TOKEN_RANGE", "TRAP_MASK_VALUE", "TRAP_ROPE_CAPACITY",
-           "EFFECT_PAD", "EFFECT_REGROW", "EFFECT_CLAMP", "FP16_MAX"]
+           "EFFECT_PAD", "EFFECT_REGROW", "EFFECT_CLAMP", "FP16_MAX",
+           "OracleDecoder", "DecodeStep", "generate_greedy", "greedy", "TRAP_KV_CAPACITY"]

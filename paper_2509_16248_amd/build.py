@@ -27,7 +27,7 @@ COMMON = ["-O3", "-fPIC", "-std=c++17", f"--offload-arch={ARCH}",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-Wno-unused-command-line-argument"]
 
-SOURCES = ["gm_rows.hip", "gm_gemm.hip", "gm_attention.hip", "gm_runtime.cpp"]
+SOURCES = ["gm_rows.hip", "gm_gemm.hip", "gm_attention.hip", "gm_decode.hip", "gm_runtime.cpp"]
 
 
 def _compile(src: str) -> str:

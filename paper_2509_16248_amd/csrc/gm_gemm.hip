@@ -107,7 +107,7 @@ __device__ __forceinline__ void epi_pair(const GemmArgs& a, int m, int nA,
     const int nr = nA - region * d;
     const int h = nr / hd, within = nr - h * hd;
     const int i = (within >> 5) * 16 + (within & 15);
-    int pos = m % a.seq;
+    int pos = a.pos ? a.pos[m] : m % a.seq;
     pos = pos < a.rope_rows ? pos : a.rope_rows - 1;
     const float* cs = a.rope_cos + static_cast<long long>(pos) * P + i;
     const float* sn = a.rope_sin + static_cast<long long>(pos) * P + i;
@@ -760,12 +760,126 @@ __global__ __launch_bounds__(256) void k_gemm_simple(GemmArgs a) {
   site_flush(a, sm);
 }
 
+// ------------------------------------------------------------ M <= 16 kernel
+// A decode step multiplies B <= 16 rows by the whole weight: the work is the
+// stream of weight bytes, so the kernel is laid out for HBM, not for MFMA.
+// Workgroup = 8 wavefronts = 32 consecutive packed weight rows (a 16-row
+// pair group for the gated and rotary epilogues); wavefront w streams rows
+// 4w .. 4w+3 with 16-byte coalesced loads, every lane covering a slice of K
+// for all MP activation rows (read through L1/L2).  The 64 lanes' partial
+// sums are reduced by a transposing butterfly (each step halves the values a
+// lane carries), the 32 x MP results meet in LDS, and wavefront 0 runs the
+// same epilogue as the tiled kernel.
+template <int NV>
+__device__ __forceinline__ float lane_transpose_sum(float (&v)[NV], int lane, int& index) {
+  index = 0;
+  static_for<0, 6>([&](auto st) {
+    constexpr int o = 32 >> decltype(st)::value;
+    constexpr int n = NV >> decltype(st)::value;
+    if constexpr (n >= 2) {
+      constexpr int half = n / 2;
+      const bool up = (lane & o) != 0;
+#pragma unroll
+      for (int j = 0; j < half; ++j) {
+        const float send = up ? v[j] : v[j + half];
+        const float keep = up ? v[j + half] : v[j];
+        v[j] = keep + __shfl_xor(send, o, 64);
+      }
+      if (up) index += half;
+    } else {
+      v[0] += __shfl_xor(v[0], o, 64);
+    }
+  });
+  return v[0];
+}
+
+template <typename T, int MP>
+__global__ __launch_bounds__(512) void k_gemm_skinny(GemmArgs a) {
+  constexpr int VN = 16 / static_cast<int>(sizeof(T));
+  constexpr int R = 4;
+  typedef typename std::conditional<sizeof(T) == 4, f32x4v, u32x4>::type V;
+  __shared__ float res[32][MP + 1];
+  const int n0 = blockIdx.x * 32;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const T* W = static_cast<const T*>(a.W);
+  const T* A = static_cast<const T*>(a.A);
+  const T* wrow[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    int n = n0 + wave * R + r;
+    n = n < a.N ? n : a.N - 1;
+    wrow[r] = W + static_cast<long long>(n) * a.ldw;
+  }
+  const T* arow[MP];
+#pragma unroll
+  for (int m = 0; m < MP; ++m) arow[m] = A + static_cast<long long>(m < a.M ? m : a.M - 1) * a.lda;
+  float acc[R * MP];
+#pragma unroll
+  for (int j = 0; j < R * MP; ++j) acc[j] = 0.f;
+#pragma unroll 2
+  for (int k = lane * VN; k < a.K; k += 64 * VN) {
+    float w[R][VN];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const V raw = *reinterpret_cast<const V*>(wrow[r] + k);
+      const T* e = reinterpret_cast<const T*>(&raw);
+#pragma unroll
+      for (int i = 0; i < VN; ++i) w[r][i] = to_f32(e[i]);
+    }
+#pragma unroll
+    for (int m = 0; m < MP; ++m) {
+      const V raw = *reinterpret_cast<const V*>(arow[m] + k);
+      const T* e = reinterpret_cast<const T*>(&raw);
+#pragma unroll
+      for (int i = 0; i < VN; ++i) {
+        const float x = to_f32(e[i]);
+#pragma unroll
+        for (int r = 0; r < R; ++r) acc[r * MP + m] = fmaf(w[r][i], x, acc[r * MP + m]);
+      }
+    }
+  }
+  int idx;
+  const float sum = lane_transpose_sum<R * MP>(acc, lane, idx);
+  // lanes that differ only in their low bits hold the same value
+  if ((lane & (64 / (R * MP) - 1)) == 0) res[wave * R + idx / MP][idx % MP] = sum;
+  __syncthreads();
+  if (wave != 0) return;
+  SiteMax sm;
+  const int m = lane >> 2, q = lane & 3;
+  if (m < MP && m < a.M) {
+    float va[4], vb[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      va[r] = res[4 * q + r][m];
+      vb[r] = res[16 + 4 * q + r][m];
+    }
+    epi_pair<T>(a, m, n0 + 4 * q, va, vb, sm);
+  }
+  site_flush(a, sm);
+}
+
+template <typename T>
+static void skinny_t(const GemmArgs& a, hipStream_t s) {
+  const dim3 grid((a.N + 31) / 32), block(512);
+  if (a.M <= 1) hipLaunchKernelGGL((k_gemm_skinny<T, 1>), grid, block, 0, s, a);
+  else if (a.M <= 2) hipLaunchKernelGGL((k_gemm_skinny<T, 2>), grid, block, 0, s, a);
+  else if (a.M <= 4) hipLaunchKernelGGL((k_gemm_skinny<T, 4>), grid, block, 0, s, a);
+  else if (a.M <= 8) hipLaunchKernelGGL((k_gemm_skinny<T, 8>), grid, block, 0, s, a);
+  else hipLaunchKernelGGL((k_gemm_skinny<T, 16>), grid, block, 0, s, a);
+}
+
 static bool g_force_simple = false;
 static int g_gemm_variant = 0;
 void gemm_force_simple(bool on) { g_force_simple = on; }
 void gemm_set_variant(int v) { g_gemm_variant = v; }
 
 void launch_gemm(const GemmArgs& a, hipStream_t s) {
+  if (a.M <= 16 && !g_force_simple) {
+    if (a.dtype == kF32) skinny_t<float>(a, s);
+    else if (a.dtype == kBF16) skinny_t<bf16_t>(a, s);
+    else skinny_t<f16_t>(a, s);
+    return;
+  }
   if (a.dtype == kF32 || g_force_simple) {
     const dim3 grid(((a.M + 63) / 64) * ((a.N + 63) / 64));
     if (a.dtype == kF32) hipLaunchKernelGGL(k_gemm_simple<float>, grid, dim3(256), 0, s, a);

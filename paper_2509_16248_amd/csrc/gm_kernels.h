@@ -31,9 +31,12 @@ struct GemmArgs {
   const void* resid; int ldr;
   int32_t* state; int site; // clamp-site reduction target (site < 0: none)
   const float* rope_cos; const float* rope_sin; int rope_rows;
-  int seq;                  // positions are m % seq
+  int seq;                  // positions are m % seq, or pos[m] when pos is set
+  const int32_t* pos;       // per-row positions (decode step), or null
   int head_dim; int d_model;
 };
+// M <= 16 rows (a decode step, or a tiny forward) runs on a weight-streaming
+// kernel; larger M on the tiled MFMA kernel.
 void launch_gemm(const GemmArgs& a, hipStream_t s);
 
 struct AttnArgs {
@@ -60,6 +63,7 @@ struct RowArgs {
   int rows, d;
   // source: embedding gather (ids != null) or a [rows, d] tensor x
   const int32_t* ids; const void* tok_emb; const void* pos_emb; int seq; int vocab;
+  const int32_t* pos;       // embedding positions per row (decode step), or null: row % seq
   void* x;                  // embedding: written with R(emb); else read (and clamped in place)
   int norm;                 // -1 none, 0 LayerNorm, 1 RMSNorm
   const void* g; const void* b; float eps;
@@ -70,6 +74,54 @@ void launch_rownorm(const RowArgs& a, hipStream_t s);
 
 void launch_emit_effects(int32_t* state, void* fifo, int fifo_cap, int n_sites,
                          hipStream_t s);
+
+// ------------------------------------------------------------ decode step
+// KV cache: per layer, K and V as [max_batch][H][max_seq][hd] (act dtype) and
+// one byte per (sequence, position) saying whether that key may be attended.
+
+// Guards and positions of one decode step (one workgroup): ids in [0, vocab)
+// (trap 1, index b), seqlen[b] < max_seq (trap 4, index b), rotary need =
+// max_b seqlen[b] + 1 <= capacity (trap 3); pos[b] = seqlen[b] (clamped);
+// rotary regrow as in the prologue; per-forward slots reset.
+void launch_decode_prologue(const int32_t* ids, int B, int vocab, int max_seq, int rotary,
+                            int capacity, int n_sites, const int32_t* seqlen, int32_t* pos,
+                            int32_t* state, hipStream_t s);
+
+struct KvArgs {
+  int dtype;
+  int rows;                 // token rows of qkv
+  int S;                    // prefill: row = b*S + s; 0 for a decode step (row b at pos[b])
+  const int32_t* pos;       // decode: [rows]
+  const int32_t* mask;      // prefill: [B, S] key validity
+  const int32_t* state;     // decode: nothing is stored when the step trapped
+  const void* qkv; int d, H, hd;
+  void* kc; void* vc;       // this layer's cache
+  uint8_t* valid;           // [max_batch][max_seq]
+  int max_seq;
+};
+void launch_kv_store(const KvArgs& a, hipStream_t s);
+
+struct DecAttnArgs {
+  int dtype;
+  int B, H, hd, d;
+  const void* qkv;          // [B, 3d]: q of sequence b at row b, head h at columns h*hd
+  const void* kc; const void* vc; const uint8_t* valid; int max_seq;
+  const int32_t* pos;       // keys 0 .. pos[b] of sequence b
+  void* ctx;                // [B, d]
+  float* part;              // [B*H*nsplit*(hd+2)] partial softmax state per key chunk
+  int nsplit, chunk;
+  float scale;
+};
+void launch_decode_attention(const DecAttnArgs& a, hipStream_t s);
+
+// next[b] = index of the largest logit of row b (first NaN if any; lowest
+// index among equal values).
+void launch_argmax(const void* logits, int dtype, int B, int V, int32_t* next, hipStream_t s);
+
+// Sequence lengths after a forward: prefill seqlen[b] = 1 + last unmasked
+// key; decode seqlen[b] = pos[b] + 1 unless the step trapped.
+void launch_seqlen_update(int32_t* seqlen, const int32_t* pos, const int32_t* state, int B,
+                          int decode, hipStream_t s);
 
 void launch_gather_rows(void* dst, const void* src, const int32_t* row_map,
                         int rows, int row_bytes, hipStream_t s);

@@ -185,8 +185,8 @@ __global__ __launch_bounds__(256) void k_rownorm(RowArgs a) {
     int id = a.ids[row];
     id = id < 0 ? 0 : (id >= a.vocab ? a.vocab - 1 : id);   // in bounds even when trapped
     const T* e = static_cast<const T*>(a.tok_emb) + static_cast<long long>(id) * d;
-    const T* p = a.pos_emb ? static_cast<const T*>(a.pos_emb) +
-                                 static_cast<long long>(row % a.seq) * d
+    const int position = a.pos ? a.pos[row] : row % a.seq;
+    const T* p = a.pos_emb ? static_cast<const T*>(a.pos_emb) + static_cast<long long>(position) * d
                            : nullptr;
 #pragma unroll
     for (int j = 0; j < MAXV; ++j) {

@@ -48,11 +48,18 @@ struct LayerBufs {
 };
 
 struct GraphEntry {
+  int kind;                 // 0 forward, 1 decode step
   int B, S;
   const void *ids, *mask;
   void* logits;
+  void* next;
   hipGraphExec_t exec;
   uint64_t last_use;
+};
+
+// A decode step's extra launch parameters.
+struct Dec {
+  int32_t* next;            // greedy token per sequence, or null
 };
 
 constexpr int kFifoCap = 4096;
@@ -88,6 +95,15 @@ struct gm_model {
   std::vector<Frag> frags;
   bool debug_sync = false;
   uint64_t tick = 0;
+  // KV cache (cfg.kv_cache): per layer K and V [max_batch][H][max_seq][hd],
+  // key validity [max_batch][max_seq], sequence lengths, decode positions and
+  // the split-key attention workspace.
+  std::vector<void*> kc, vc;
+  uint8_t* kv_valid = nullptr;
+  int32_t *seqlen = nullptr, *dpos = nullptr;
+  float* dpart = nullptr;
+  int dec_nsplit = 0, dec_chunk = 0;
+  int cache_B = 0;          // batch of the last prefill (host-side), 0 = none
 
   int alloc(void** p, size_t bytes) {
     *p = nullptr;
@@ -140,6 +156,10 @@ int validate(const gm_config* c) {
     if (c->act_dtype != GM_DTYPE_F16) return inval("fp16_clamp needs act_dtype f16");
     if (c->norm_place != GM_NORM_PRE) return inval("fp16_clamp needs pre-norm");
     if (!(c->clamp_margin >= 0.f) || c->clamp_margin >= 65504.f) return inval("bad clamp_margin");
+  }
+  if (c->kv_cache) {
+    if (!c->causal) return inval("kv_cache needs a causal model");
+    if (c->fp16_clamp) return inval("kv_cache is not supported with fp16_clamp");
   }
   return GM_OK;
 }
@@ -247,8 +267,12 @@ struct Seg {
 };
 constexpr int kCountOnly = -2;
 
+// One forward (dec == null: B x S tokens, with the KV cache filled when the
+// model has one) or one decode step (dec != null: S == 1, one new token per
+// sequence at position seqlen[b], attending to the cache).
 void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
-             void* logits, hipStream_t s, Prof* prof = nullptr, Seg* seg = nullptr) {
+             void* logits, hipStream_t s, Prof* prof = nullptr, Seg* seg = nullptr,
+             const Dec* dec = nullptr) {
   const gm_config& c = m->cfg;
   auto on = [&]() { return !seg || seg->want == -1 || seg->want == seg->cur; };
   auto brk = [&]() {
@@ -266,7 +290,10 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
     if (prof) prof->mark(kind, layer, flops, bytes);
   };
   if (prof) prof->start();
-  if (on())
+  if (dec)
+    launch_decode_prologue(ids, B, c.vocab, c.max_seq, c.pos == GM_POS_ROTARY, c.rope_capacity,
+                           ns, m->seqlen, m->dpos, m->state, s);
+  else if (on())
     launch_prologue(ids, mask, B, S, c.vocab, c.pos == GM_POS_ROTARY, c.rope_capacity, ns,
                     m->state, s);
   P(GM_K_PROLOGUE, -1, 0.0, 8.0 * T);
@@ -288,6 +315,7 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
   r.tok_emb = m->tok_emb;
   r.pos_emb = c.pos == GM_POS_LEARNED ? m->pos_emb : nullptr;
   r.seq = S;
+  r.pos = dec ? m->dpos : nullptr;
   r.vocab = c.vocab;
   r.x = m->h;
   r.norm = c.emb_norm ? normk : -1;
@@ -317,6 +345,7 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
   ga.state = m->state;
   ga.site = -1;
   ga.seq = S;
+  ga.pos = dec ? m->dpos : nullptr;
   ga.head_dim = hd;
   ga.d_model = d;
   ga.rope_cos = m->rope_cos;
@@ -367,7 +396,50 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
   const double pairs = c.causal ? 0.5 * S * (S + 1.0) : static_cast<double>(S) * S;
   const double attn_flops = 4.0 * hd * pairs * B * c.n_heads;
   const double attn_bytes = es * (static_cast<double>(T) * 3 * d + static_cast<double>(T) * d);
+  KvArgs kv{};
+  kv.dtype = m->dtype;
+  kv.rows = T;
+  kv.S = dec ? 0 : S;
+  kv.pos = m->dpos;
+  kv.mask = mask;
+  kv.state = m->state;
+  kv.qkv = m->qkv;
+  kv.d = d;
+  kv.H = c.n_heads;
+  kv.hd = hd;
+  kv.valid = m->kv_valid;
+  kv.max_seq = c.max_seq;
+  DecAttnArgs da{};
+  da.dtype = m->dtype;
+  da.B = B;
+  da.H = c.n_heads;
+  da.hd = hd;
+  da.d = d;
+  da.qkv = m->qkv;
+  da.valid = m->kv_valid;
+  da.max_seq = c.max_seq;
+  da.pos = m->dpos;
+  da.ctx = m->ctx;
+  da.part = m->dpart;
+  da.nsplit = m->dec_nsplit;
+  da.chunk = m->dec_chunk;
+  da.scale = at.scale;
   auto attention = [&]() {
+    if (c.kv_cache) {
+      // this layer's k and v go to the cache (prefill: every position; decode: pos[b])
+      kv.kc = m->kc[cur_layer];
+      kv.vc = m->vc[cur_layer];
+      if (on()) launch_kv_store(kv, s);
+      P(GM_K_KV_STORE, cur_layer, 0.0, 4.0 * T * d * es);
+    }
+    if (dec) {
+      da.kc = m->kc[cur_layer];
+      da.vc = m->vc[cur_layer];
+      launch_decode_attention(da, s);
+      const double keys = static_cast<double>(B) * c.max_seq;   // upper bound: full cache
+      P(GM_K_ATTENTION, cur_layer, 4.0 * hd * keys * c.n_heads, es * 2.0 * keys * d);
+      return;
+    }
     if (on()) launch_attention(at, s);
     P(GM_K_ATTENTION, cur_layer, attn_flops, attn_bytes);
   };
@@ -402,11 +474,67 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
     z = m->a;
   }
   gemm(GM_K_GEMM_HEAD, z, d, m->head, c.vocab, kEpiStore, nullptr, logits, c.vocab, nullptr, -1);
+  if (dec && dec->next) {
+    launch_argmax(logits, m->dtype, B, c.vocab, dec->next, s);
+    P(GM_K_ARGMAX, -1, 0.0, es * B * static_cast<double>(c.vocab));
+  }
+  if (c.kv_cache && on()) launch_seqlen_update(m->seqlen, m->dpos, m->state, B, dec ? 1 : 0, s);
   if (on()) launch_emit_effects(m->state, m->fifo, kFifoCap, ns, s);
   P(GM_K_EFFECTS, -1, 0.0, 0.0);
 }
 
 }  // namespace
+
+// Launch the graph cached for `key` (kind, shape and buffer pointers),
+// capturing and instantiating it first on a cold key (LRU of kMaxGraphs).
+template <typename Body>
+int launch_graph(gm_model* m, GraphEntry key, hipStream_t stream, Body body) {
+  GraphEntry* ge = nullptr;
+  for (auto& g : m->graphs)
+    if (g.kind == key.kind && g.B == key.B && g.S == key.S && g.ids == key.ids &&
+        g.mask == key.mask && g.logits == key.logits && g.next == key.next)
+      ge = &g;
+  if (!ge) {
+    hipGraph_t graph = nullptr;
+    HIP_TRY(hipStreamBeginCapture(m->cap_stream, hipStreamCaptureModeThreadLocal));
+    body(m->cap_stream);
+    hipError_t e = hipStreamEndCapture(m->cap_stream, &graph);
+    if (e != hipSuccess || !graph) {
+      g_last_error = std::string("capture: ") + hipGetErrorString(e);
+      hipGetLastError();
+      return GM_E_CAPTURE;
+    }
+    size_t nodes = 0;
+    hipGraphGetNodes(graph, nullptr, &nodes);
+    hipGraphExec_t exec = nullptr;
+    e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+    hipGraphDestroy(graph);
+    if (e != hipSuccess) {
+      g_last_error = std::string("instantiate: ") + hipGetErrorString(e);
+      return GM_E_CAPTURE;
+    }
+    if (static_cast<int>(m->graphs.size()) >= kMaxGraphs) {
+      size_t victim = 0;
+      for (size_t i = 1; i < m->graphs.size(); ++i)
+        if (m->graphs[i].last_use < m->graphs[victim].last_use) victim = i;
+      hipGraphExecDestroy(m->graphs[victim].exec);
+      m->graphs.erase(m->graphs.begin() + victim);
+    }
+    key.exec = exec;
+    m->graphs.push_back(key);
+    ge = &m->graphs.back();
+    m->stats.captures++;
+    m->stats.kernels_per_forward = nodes;
+  }
+  ge->last_use = ++m->tick;
+  HIP_TRY(hipGraphLaunch(ge->exec, stream));
+  m->stats.graph_launches++;
+  if (m->debug_sync) {
+    m->stats.host_syncs_in_forward++;
+    HIP_TRY(hipStreamSynchronize(stream));
+  }
+  return GM_OK;
+}
 
 extern "C" {
 
@@ -534,6 +662,32 @@ int gm_model_create(const gm_config* cfg, const gm_weights* w, gm_model** out) {
       (rc = m->alloc(&m->f, T * ff * es)) ||
       (!pre && (rc = m->alloc(&m->tmp, T * d * es))))
     return fail(rc);
+  if (c.kv_cache) {
+    const size_t per_layer = static_cast<size_t>(c.max_batch) * c.max_seq * d * es;
+    m->kc.assign(c.n_layers, nullptr);
+    m->vc.assign(c.n_layers, nullptr);
+    for (int l = 0; l < c.n_layers; ++l)
+      if ((rc = m->alloc(&m->kc[l], per_layer)) || (rc = m->alloc(&m->vc[l], per_layer)))
+        return fail(rc);
+    // keys per split chunk: a multiple of 64, at most 32 chunks
+    m->dec_chunk = 64 * ((c.max_seq + 64 * 32 - 1) / (64 * 32));
+    m->dec_nsplit = (c.max_seq + m->dec_chunk - 1) / m->dec_chunk;
+    void* q = nullptr;
+    if ((rc = m->alloc(&q, static_cast<size_t>(c.max_batch) * c.max_seq))) return fail(rc);
+    m->kv_valid = static_cast<uint8_t*>(q);
+    if ((rc = m->alloc(&q, c.max_batch * sizeof(int32_t)))) return fail(rc);
+    m->seqlen = static_cast<int32_t*>(q);
+    if ((rc = m->alloc(&q, c.max_batch * sizeof(int32_t)))) return fail(rc);
+    m->dpos = static_cast<int32_t*>(q);
+    if ((rc = m->alloc(&q, static_cast<size_t>(c.max_batch) * c.n_heads * m->dec_nsplit * (hd + 2) *
+                                sizeof(float))))
+      return fail(rc);
+    m->dpart = static_cast<float*>(q);
+    e = hipMemset(m->kv_valid, 0, static_cast<size_t>(c.max_batch) * c.max_seq);
+    if (e == hipSuccess) e = hipMemset(m->seqlen, 0, c.max_batch * sizeof(int32_t));
+    if (e == hipSuccess) e = hipMemset(m->dpos, 0, c.max_batch * sizeof(int32_t));
+    if (e != hipSuccess) return fail(hip_fail(e, "hipMemset"));
+  }
   // device state
   m->n_state = kKvLenBase + c.max_batch;
   void* p = nullptr;
@@ -675,6 +829,7 @@ int gm_forward_ex(gm_model* m, int32_t B, int32_t S, const int32_t* ids, const i
   if (B < 1 || B > m->cfg.max_batch || S < 1 || S > m->cfg.max_seq)
     return inval("B or S out of range");
   m->stats.forwards++;
+  if (m->cfg.kv_cache) m->cache_B = B;   // the forward fills the cache for these B sequences
   if (m->exec_mode == GM_EXEC_FRAGMENTED) return forward_fragmented(m, B, S, ids, mask, logits, stream);
   if (m->exec_mode == GM_EXEC_EAGER) {
     enqueue(m, B, S, ids, mask, logits, stream);
@@ -686,48 +841,36 @@ int gm_forward_ex(gm_model* m, int32_t B, int32_t S, const int32_t* ids, const i
     }
     return GM_OK;
   }
-  GraphEntry* ge = nullptr;
-  for (auto& g : m->graphs)
-    if (g.B == B && g.S == S && g.ids == ids && g.mask == mask && g.logits == logits) ge = &g;
-  if (!ge) {
-    hipGraph_t graph = nullptr;
-    HIP_TRY(hipStreamBeginCapture(m->cap_stream, hipStreamCaptureModeThreadLocal));
-    enqueue(m, B, S, ids, mask, logits, m->cap_stream);
-    hipError_t e = hipStreamEndCapture(m->cap_stream, &graph);
-    if (e != hipSuccess || !graph) {
-      g_last_error = std::string("capture: ") + hipGetErrorString(e);
-      hipGetLastError();
-      return GM_E_CAPTURE;
+  return launch_graph(m, GraphEntry{0, B, S, ids, mask, logits, nullptr, nullptr, 0}, stream,
+                      [&](hipStream_t cs) { enqueue(m, B, S, ids, mask, logits, cs); });
+}
+
+int gm_decode_step(gm_model* m, int32_t B, const int32_t* ids, void* logits, int32_t* next,
+                   hipStream_t stream) {
+  if (!m) return inval("model is NULL");
+  if (!ids || !logits) return inval("ids and logits must be non-NULL");
+  if ((reinterpret_cast<uintptr_t>(ids) | reinterpret_cast<uintptr_t>(logits) |
+       reinterpret_cast<uintptr_t>(next)) & 15)
+    return inval("ids, logits and next must be 16-byte aligned");
+  if (!m->cfg.kv_cache) return inval("the model was created without kv_cache");
+  if (m->cache_B == 0) return inval("no prefill (gm_forward_ex) has filled the KV cache");
+  if (B != m->cache_B) return inval("B must equal the batch of the last prefill");
+  if (m->exec_mode == GM_EXEC_FRAGMENTED)
+    return inval("fragmented execution covers gm_forward only");
+  m->stats.decode_steps++;
+  const Dec dec{next};
+  if (m->exec_mode == GM_EXEC_EAGER) {
+    enqueue(m, B, 1, ids, nullptr, logits, stream, nullptr, nullptr, &dec);
+    HIP_TRY(hipGetLastError());
+    m->stats.eager_forwards++;
+    if (m->debug_sync) {
+      m->stats.host_syncs_in_forward++;
+      HIP_TRY(hipStreamSynchronize(stream));
     }
-    size_t nodes = 0;
-    hipGraphGetNodes(graph, nullptr, &nodes);
-    hipGraphExec_t exec = nullptr;
-    e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
-    hipGraphDestroy(graph);
-    if (e != hipSuccess) {
-      g_last_error = std::string("instantiate: ") + hipGetErrorString(e);
-      return GM_E_CAPTURE;
-    }
-    if (static_cast<int>(m->graphs.size()) >= kMaxGraphs) {
-      size_t victim = 0;
-      for (size_t i = 1; i < m->graphs.size(); ++i)
-        if (m->graphs[i].last_use < m->graphs[victim].last_use) victim = i;
-      hipGraphExecDestroy(m->graphs[victim].exec);
-      m->graphs.erase(m->graphs.begin() + victim);
-    }
-    m->graphs.push_back(GraphEntry{B, S, ids, mask, logits, exec, 0});
-    ge = &m->graphs.back();
-    m->stats.captures++;
-    m->stats.kernels_per_forward = nodes;
+    return GM_OK;
   }
-  ge->last_use = ++m->tick;
-  HIP_TRY(hipGraphLaunch(ge->exec, stream));
-  m->stats.graph_launches++;
-  if (m->debug_sync) {
-    m->stats.host_syncs_in_forward++;
-    HIP_TRY(hipStreamSynchronize(stream));
-  }
-  return GM_OK;
+  return launch_graph(m, GraphEntry{1, B, 1, ids, nullptr, logits, next, nullptr, 0}, stream,
+                      [&](hipStream_t cs) { enqueue(m, B, 1, ids, nullptr, logits, cs, nullptr, nullptr, &dec); });
 }
 
 int gm_profile_forward(gm_model* m, int32_t B, int32_t S, const int32_t* ids,

@@ -13,7 +13,7 @@ from typing import Callable, List, Optional
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libgm.so")
 
-GM_ABI_VERSION = 1
+GM_ABI_VERSION = 2
 GM_MAX_LAYERS = 64
 GM_OK, GM_E_INVAL, GM_E_NOMEM, GM_E_HIP, GM_E_CAPTURE, GM_E_TRAP = 0, -1, -2, -3, -4, -5
 GM_EXEC_GRAPH, GM_EXEC_EAGER, GM_EXEC_FRAGMENTED = 0, 1, 2
@@ -23,6 +23,7 @@ GM_NORM_PRE, GM_NORM_POST = 0, 1
 GM_FFN_GELU, GM_FFN_GEGLU, GM_FFN_SWIGLU = 0, 1, 2
 GM_POS_NONE, GM_POS_LEARNED, GM_POS_ROTARY = 0, 1, 2
 GM_TRAP_NONE, GM_TRAP_TOKEN_RANGE, GM_TRAP_MASK_VALUE, GM_TRAP_ROPE_CAPACITY = 0, 1, 2, 3
+GM_TRAP_KV_CAPACITY = 4
 GM_EFFECT_PAD, GM_EFFECT_REGROW, GM_EFFECT_CLAMP = 1, 2, 3
 
 _i32, _f32, _u64, _vp = ctypes.c_int32, ctypes.c_float, ctypes.c_uint64, ctypes.c_void_p
@@ -36,7 +37,8 @@ class gm_config(ctypes.Structure):
                 ("pos", _i32), ("causal", _i32), ("has_bias", _i32),
                 ("tied_head", _i32), ("norm_eps", _f32), ("rope_base", _f32),
                 ("rope_init_len", _i32), ("rope_capacity", _i32),
-                ("act_dtype", _i32), ("fp16_clamp", _i32), ("clamp_margin", _f32)]
+                ("act_dtype", _i32), ("fp16_clamp", _i32), ("clamp_margin", _f32),
+                ("kv_cache", _i32)]
 
 
 LAYER_FIELDS = ["ln1_g", "ln1_b", "wqkv", "bqkv", "wo", "bo", "ln2_g", "ln2_b",
@@ -69,7 +71,7 @@ class gm_effect(ctypes.Structure):
 class gm_stats(ctypes.Structure):
     _fields_ = [("forwards", _u64), ("captures", _u64), ("graph_launches", _u64),
                 ("eager_forwards", _u64), ("host_syncs_in_forward", _u64),
-                ("kernels_per_forward", _u64)]
+                ("kernels_per_forward", _u64), ("decode_steps", _u64)]
 
 
 class gm_kernel_time(ctypes.Structure):
@@ -78,11 +80,13 @@ class gm_kernel_time(ctypes.Structure):
 
 
 KERNEL_KINDS = ["prologue", "rope_fill", "embed", "norm", "gemm_qkv", "attention",
-                "gemm_o", "gemm_up", "gemm_down", "gemm_head", "effects"]
+                "gemm_o", "gemm_up", "gemm_down", "gemm_head", "effects", "kv_store",
+                "argmax"]
 
 gm_effect_cb = ctypes.CFUNCTYPE(None, ctypes.POINTER(gm_effect), ctypes.c_void_p)
 
 EXPORTS = ["gm_model_create", "gm_model_destroy", "gm_forward", "gm_forward_ex",
+           "gm_decode_step",
            "gm_profile_forward", "gm_set_exec_mode", "gm_set_graph_mode", "gm_read_decisions", "gm_decisions_device_ptr",
            "gm_check_error", "gm_flush_effects", "gm_debug_buffer", "gm_get_stats",
            "gm_strerror",
@@ -106,6 +110,7 @@ def lib(path: str = LIB_PATH) -> ctypes.CDLL:
     L.gm_model_destroy.restype = None
     L.gm_forward.argtypes = [_vp, _vp, _vp, _vp, _vp]
     L.gm_forward_ex.argtypes = [_vp, _i32, _i32, _vp, _vp, _vp, _vp]
+    L.gm_decode_step.argtypes = [_vp, _i32, _vp, _vp, _vp, _vp]
     L.gm_set_graph_mode.argtypes = [_vp, _i32]
     L.gm_set_exec_mode.argtypes = [_vp, _i32]
     L.gm_profile_forward.argtypes = [_vp, _i32, _i32, _vp, _vp, _vp, _vp,
@@ -161,6 +166,11 @@ def gm_forward(m: int, ids: int, mask: int, logits: int, stream: int) -> None:
 
 def gm_forward_ex(m: int, B: int, S: int, ids: int, mask: int, logits: int, stream: int) -> None:
     _check(lib().gm_forward_ex(m, B, S, ids, mask, logits, stream), "gm_forward_ex")
+
+
+def gm_decode_step(m: int, B: int, ids: int, logits: int, next_ids: Optional[int],
+                   stream: int) -> None:
+    _check(lib().gm_decode_step(m, B, ids, logits, next_ids, stream), "gm_decode_step")
 
 
 def gm_profile_forward(m: int, B: int, S: int, ids: int, mask: int, logits: int,

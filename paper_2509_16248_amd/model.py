@@ -19,7 +19,8 @@ _FFN = {"gelu": gm.GM_FFN_GELU, "geglu": gm.GM_FFN_GEGLU, "swiglu": gm.GM_FFN_SW
 _POS = {"none": gm.GM_POS_NONE, "learned": gm.GM_POS_LEARNED, "rotary": gm.GM_POS_ROTARY}
 
 
-def make_config(c, max_batch: Optional[int] = None, max_seq: Optional[int] = None) -> gm.gm_config:
+def make_config(c, max_batch: Optional[int] = None, max_seq: Optional[int] = None,
+                kv_cache: bool = False) -> gm.gm_config:
     """gm_config from any object with the workload attributes (n_layers,
     d_model, n_heads, d_ff, vocab, batch, seq, dtype, norm, norm_place,
     emb_norm, ffn, pos, causal, bias, tied_head, norm_eps, rope_*,
@@ -33,7 +34,7 @@ def make_config(c, max_batch: Optional[int] = None, max_seq: Optional[int] = Non
         tied_head=int(c.tied_head), norm_eps=c.norm_eps, rope_base=c.rope_base,
         rope_init_len=c.rope_init_len, rope_capacity=c.rope_capacity,
         act_dtype=_DTYPES[c.dtype], fp16_clamp=int(c.fp16_clamp),
-        clamp_margin=c.clamp_margin)
+        clamp_margin=c.clamp_margin, kv_cache=int(kv_cache))
 
 
 def to_device(a: np.ndarray, dtype: str, device) -> torch.Tensor:
@@ -52,10 +53,11 @@ class GmModel:
     device tensors) named as in gm_weights / gm_layer_weights."""
 
     def __init__(self, cfg, globals_: Dict, layers: List[Dict], device="cuda",
-                 max_batch: Optional[int] = None, max_seq: Optional[int] = None):
+                 max_batch: Optional[int] = None, max_seq: Optional[int] = None,
+                 kv_cache: bool = False):
         self.cfg = cfg
         self.device = torch.device(device)
-        self.c = make_config(cfg, max_batch, max_seq)
+        self.c = make_config(cfg, max_batch, max_seq, kv_cache)
         dt = cfg.dtype
 
         def dev(x):
@@ -97,6 +99,24 @@ class GmModel:
         gm.gm_forward_ex(self.handle, B, S, ids.data_ptr(), mask.data_ptr(),
                          logits.data_ptr(), self._stream(stream))
         return logits
+
+    def decode(self, ids: torch.Tensor, logits: torch.Tensor,
+               next_ids: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+        """One gm_decode_step: ids [B] int32 (device), logits [B, vocab];
+        next_ids [B] int32 receives the greedy tokens (may be ``ids``)."""
+        (B,) = ids.shape
+        assert ids.dtype == torch.int32 and ids.is_contiguous()
+        assert logits.shape == (B, self.c.vocab) and logits.is_contiguous()
+        assert logits.dtype == _TORCH[self.cfg.dtype]
+        if next_ids is not None:
+            assert next_ids.shape == (B,) and next_ids.dtype == torch.int32
+        gm.gm_decode_step(self.handle, B, ids.data_ptr(), logits.data_ptr(),
+                          next_ids.data_ptr() if next_ids is not None else None,
+                          self._stream(stream))
+        return logits
+
+    def new_decode_logits(self, B: int) -> torch.Tensor:
+        return torch.empty((B, self.c.vocab), dtype=_TORCH[self.cfg.dtype], device=self.device)
 
     def profile(self, ids: torch.Tensor, mask: torch.Tensor, logits: torch.Tensor, stream=None):
         """Per-launch timing of one eager forward (see gm_profile_forward)."""
