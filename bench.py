@@ -100,6 +100,63 @@ def break_suite(args):
         torch.cuda.empty_cache()
 
 
+def decode_bench(cfg, w, prompt=384, steps=120, warmup=8):
+    """Greedy decoding with the KV cache on the benchmarked model: prefill
+    B x ``prompt`` positions (ragged, 0..128 trailing pads), then ``steps``
+    decode steps in which each step's greedy tokens (device argmax) are the
+    next step's input, one graph launch per step and no host read.  The
+    step is HBM-bound: its algorithmic bytes are every weight read once plus
+    the cached keys and values of every sequence up to its position."""
+    import numpy as np
+    import torch
+    import synth
+    from paper_2509_16248_amd.model import GmModel
+    B = cfg.batch
+    m = GmModel(cfg, w.globals, w.layers, device="cuda:0", kv_cache=True)
+    ids, mask = synth.make_inputs(cfg, 3, seq=prompt)
+    ids_t = torch.from_numpy(ids).cuda()
+    mask_t = torch.from_numpy(mask).cuda()
+    out = m.new_logits(B, prompt)
+    tok = torch.ones(B, dtype=torch.int32, device="cuda")
+    logits = m.new_decode_logits(B)
+    stream = torch.cuda.current_stream()
+    for _ in range(2):                     # cold captures: prefill and step graphs
+        m.forward(ids_t, mask_t, out)
+        for _ in range(warmup):
+            m.decode(tok, logits, tok)
+    torch.cuda.synchronize()
+    m.forward(ids_t, mask_t, out)
+    tok.fill_(1)
+    s0 = m.stats()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    for _ in range(steps):
+        m.decode(tok, logits, tok)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / steps
+    s1 = m.stats()
+    code = m.check_error()
+    m.close()
+    L0 = mask.sum(1).astype(np.int64)            # lengths before the first step
+    d, ff, V, nl = cfg.d_model, cfg.d_ff, cfg.vocab, cfg.n_layers
+    up = 2 * ff if cfg.gated else ff
+    weight_bytes = 2.0 * (nl * (3 * d * d + d * d + up * d + d * ff) + V * d)
+    # keys and values read per step, averaged over the timed steps
+    kv_bytes = 2.0 * 2 * nl * d * float(np.mean([(L0 + t + 1).sum() for t in range(steps)]))
+    gbs = (weight_bytes + kv_bytes) / (ms * 1e-3) / 1e9
+    return {"workload": f"{cfg.name}: batch {B}, prompts of {prompt} positions with 0..{cfg.max_pad} "
+                        f"trailing pads, {steps} greedy steps (device argmax fed back)",
+            "ms_per_step": round(ms, 4), "tokens_per_s": round(B / (ms * 1e-3), 1),
+            "graph_launches_per_step": (s1["graph_launches"] - s0["graph_launches"]) / steps,
+            "host_syncs_per_step": (s1["host_syncs_in_forward"] - s0["host_syncs_in_forward"]) / steps,
+            "trap": list(code),
+            "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
+                         "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
+                         "bytes_per_step": weight_bytes + kv_bytes}}
+
+
 def measured_traffic():
     """HBM bytes per GEMM launch from the committed rocprofv3 FETCH_SIZE /
     WRITE_SIZE summary, if it was taken on the GEMM source as it is now."""
@@ -142,6 +199,7 @@ def main():
     ap.add_argument("--cpu-rows", type=int, default=2)
     ap.add_argument("--no-fragmented", action="store_true",
                     help="skip the graph-broken baseline (same kernels, host sync per break)")
+    ap.add_argument("--no-decode", action="store_true", help="skip the KV-cache decode measurement")
     ap.add_argument("--break-suite", action="store_true",
                     help="only compare single-graph and graph-broken forwards on every workload")
     args = ap.parse_args()
@@ -254,6 +312,10 @@ def main():
         result["fragmented_baseline"] = fragmented(m, ids_t, mask_t, args)
         log(f"[bench] single graph vs graph-broken: {result['fragmented_baseline']}")
     m.close()
+    if not args.no_decode:
+        torch.cuda.empty_cache()
+        result["decode"] = decode_bench(cfg, w)
+        log(f"[bench] decode: {result['decode']}")
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a sample")
         result["cpu_baseline"] = cpu_baseline(cfg, w, ids, mask, list(range(args.cpu_rows)))

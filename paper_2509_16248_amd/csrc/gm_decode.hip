@@ -131,9 +131,13 @@ void launch_kv_store(const KvArgs& a, hipStream_t s) {
 // G = hd/VN lanes hold one key row (16 bytes each), so a wavefront handles
 // 64/G keys per step; each lane group keeps an online softmax (max m, sum l,
 // unnormalised output o over its VN dimensions).  The groups are merged in
-// LDS and the chunk's (m, l, o) goes to the workspace; k_decode_combine
-// merges the chunks and normalises.  Keys marked invalid get weight 0; a
-// sequence without a valid key gets a zero context.
+// LDS; with one chunk per head the workgroup normalises and writes the
+// context, otherwise the chunk's (m, l, o) goes to the workspace and
+// k_decode_combine merges the chunks.  (A last-workgroup-merges ticket would
+// save that launch but needs a device-scope fence per workgroup, which on
+// this GPU writes back the XCD's whole L2: far slower than the launch.)
+// Keys marked invalid get weight 0; a sequence without a valid key gets a
+// zero context.
 template <typename T, int HD>
 __global__ __launch_bounds__(256) void k_decode_attn(DecAttnArgs a) {
   constexpr int VN = 16 / static_cast<int>(sizeof(T));
@@ -166,24 +170,39 @@ __global__ __launch_bounds__(256) void k_decode_attn(DecAttnArgs a) {
   float m = -INFINITY, l = 0.f, o[VN];
 #pragma unroll
   for (int i = 0; i < VN; ++i) o[i] = 0.f;
-  for (int j = k0 + wave * KPW + grp; j < k1; j += NG) {
-    const V kr = *reinterpret_cast<const V*>(kc + static_cast<long long>(j) * HD);
-    const T* ke = reinterpret_cast<const T*>(&kr);
-    float s = 0.f;
+  // U keys per lane group per trip, their K and V rows loaded up front so
+  // that the loads of U keys are in flight together
+  constexpr int U = 4;
+  for (int j0 = k0 + wave * KPW + grp; j0 < k1; j0 += U * NG) {
+    V kr[U], vr[U];
+    bool ok[U];
 #pragma unroll
-    for (int i = 0; i < VN; ++i) s += q[i] * to_f32(ke[i]);
+    for (int u = 0; u < U; ++u) {
+      const int j = j0 + u * NG;
+      ok[u] = j < k1;
+      const int jj = ok[u] ? j : k1 - 1;
+      kr[u] = *reinterpret_cast<const V*>(kc + static_cast<long long>(jj) * HD);
+      vr[u] = *reinterpret_cast<const V*>(vc + static_cast<long long>(jj) * HD);
+      ok[u] = ok[u] && valid[jj];
+    }
 #pragma unroll
-    for (int off = G / 2; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
-    if (!valid[j]) continue;                   // the same for the whole lane group
-    s *= a.scale;
-    const float mn = fmaxf(m, s);
-    const float corr = expf(m - mn), p = expf(s - mn);
-    const V vr = *reinterpret_cast<const V*>(vc + static_cast<long long>(j) * HD);
-    const T* ve = reinterpret_cast<const T*>(&vr);
-    l = l * corr + p;
+    for (int u = 0; u < U; ++u) {
+      const T* ke = reinterpret_cast<const T*>(&kr[u]);
+      float s = 0.f;
 #pragma unroll
-    for (int i = 0; i < VN; ++i) o[i] = o[i] * corr + p * to_f32(ve[i]);
-    m = mn;
+      for (int i = 0; i < VN; ++i) s += q[i] * to_f32(ke[i]);
+#pragma unroll
+      for (int off = G / 2; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
+      if (!ok[u]) continue;                    // the same for the whole lane group
+      s *= a.scale;
+      const float mn = fmaxf(m, s);
+      const float corr = expf(m - mn), p = expf(s - mn);
+      const T* ve = reinterpret_cast<const T*>(&vr[u]);
+      l = l * corr + p;
+#pragma unroll
+      for (int i = 0; i < VN; ++i) o[i] = o[i] * corr + p * to_f32(ve[i]);
+      m = mn;
+    }
   }
   const int gi = wave * KPW + grp;
   if (gl == 0) {
@@ -194,6 +213,7 @@ __global__ __launch_bounds__(256) void k_decode_attn(DecAttnArgs a) {
   for (int i = 0; i < VN; ++i) s_o[gi][gl * VN + i] = o[i];
   __syncthreads();
   float* part = a.part + ((static_cast<long long>(bh) * a.nsplit) + split) * (HD + 2);
+  T* ctx = static_cast<T*>(a.ctx) + static_cast<long long>(b) * a.d + h * HD;
   for (int i = threadIdx.x; i < HD; i += blockDim.x) {
     float M = -INFINITY;
     for (int g2 = 0; g2 < NG; ++g2) M = fmaxf(M, s_m[g2]);
@@ -205,6 +225,10 @@ __global__ __launch_bounds__(256) void k_decode_attn(DecAttnArgs a) {
         L += s_l[g2] * w;
         O += s_o[g2][i] * w;
       }
+    if (a.nsplit == 1) {                 // one chunk: normalise here
+      ctx[i] = from_f32<T>(L > 0.f ? O / L : 0.f);
+      continue;
+    }
     part[2 + i] = O;
     if (i == 0) {
       part[0] = M;
@@ -236,7 +260,8 @@ __global__ __launch_bounds__(HD) void k_decode_combine(DecAttnArgs a) {
 template <typename T, int HD>
 static void decode_attn_t(const DecAttnArgs& a, hipStream_t s) {
   hipLaunchKernelGGL((k_decode_attn<T, HD>), dim3(a.B * a.H, a.nsplit), dim3(256), 0, s, a);
-  hipLaunchKernelGGL((k_decode_combine<T, HD>), dim3(a.B * a.H), dim3(HD), 0, s, a);
+  if (a.nsplit > 1)
+    hipLaunchKernelGGL((k_decode_combine<T, HD>), dim3(a.B * a.H), dim3(HD), 0, s, a);
 }
 
 template <typename T>

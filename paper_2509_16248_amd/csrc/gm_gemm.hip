@@ -75,6 +75,21 @@ struct SiteMax {
   }
 };
 
+// Decode step: four consecutive output columns n..n+3 of row b in the k
+// (region 1) or v (region 2) block of q|k|v also go to the KV cache.
+template <typename T>
+__device__ __forceinline__ void cache4(const GemmArgs& a, int b, int n, const float* v) {
+  const int d = a.d_model, region = n / d;
+  if (region < 1 || region > 2) return;
+  if (static_cast<uint32_t>(a.state[kTrapFwd]) != kTrapNone) return;
+  const int c = n - region * d, h = c / a.head_dim, i = c - h * a.head_dim;
+  const int p = a.pos[b];
+  T* dst = static_cast<T*>(region == 1 ? a.kc : a.vc) +
+           ((static_cast<long long>(b) * a.heads + h) * a.kv_max_seq + p) * a.head_dim + i;
+  store4(dst, v, 4, true);
+  if (region == 1 && c == 0) a.kv_valid[static_cast<long long>(b) * a.kv_max_seq + p] = 1;
+}
+
 // Four consecutive packed columns nA..nA+3 (first tile of a pair, values
 // va) and nA+16..nA+19 (second tile, values vb) of output row m.
 template <typename T>
@@ -126,6 +141,10 @@ __device__ __forceinline__ void epi_pair(const GemmArgs& a, int m, int nA,
     const bool vec = (a.ldo & 3) == 0;
     store4(out + base, o1, 4, vec);
     store4(out + base + P, o2, 4, vec);
+    if (a.kc && region == 1) {
+      cache4<T>(a, m, d + h * hd + i, o1);
+      cache4<T>(a, m, d + h * hd + i + P, o2);
+    }
     return;
   }
   // independent columns: store / gelu / residual (and v of kEpiRope)
@@ -158,6 +177,7 @@ __device__ __forceinline__ void epi_pair(const GemmArgs& a, int m, int nA,
           if (r < nvalid) sm.add(round_as<T>(y[r]));
     }
     store4(out + orow + n0, y, nvalid, vec);
+    if (a.kc) cache4<T>(a, m, n0, y);
   }
 }
 
@@ -353,7 +373,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm_x(GemmArgs a) {
   }
 
   SiteMax sm;
-  if (STAGE && (a.epi == kEpiStore || a.epi == kEpiGelu || a.epi == kEpiResid)) {
+  if (STAGE && !a.kc && (a.epi == kEpiStore || a.epi == kEpiGelu || a.epi == kEpiResid)) {
     // Column-independent epilogues go through LDS: bias (and GELU) are
     // applied in registers, the fp32 tile is staged, and rows are then
     // written by consecutive lanes on consecutive columns: 16-byte chunks
@@ -602,7 +622,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm_dma(GemmArgs a) {
   __syncthreads();
 
   SiteMax sm;
-  if (STAGE && (a.epi == kEpiStore || a.epi == kEpiGelu || a.epi == kEpiResid)) {
+  if (STAGE && !a.kc && (a.epi == kEpiStore || a.epi == kEpiGelu || a.epi == kEpiResid)) {
     float* st = reinterpret_cast<float*>(smem);
     const T* bias = static_cast<const T*>(a.bias);
     static_for<0, TM>([&](auto i) {
@@ -763,13 +783,14 @@ __global__ __launch_bounds__(256) void k_gemm_simple(GemmArgs a) {
 // ------------------------------------------------------------ M <= 16 kernel
 // A decode step multiplies B <= 16 rows by the whole weight: the work is the
 // stream of weight bytes, so the kernel is laid out for HBM, not for MFMA.
-// Workgroup = 8 wavefronts = 32 consecutive packed weight rows (a 16-row
-// pair group for the gated and rotary epilogues); wavefront w streams rows
-// 4w .. 4w+3 with 16-byte coalesced loads, every lane covering a slice of K
-// for all MP activation rows (read through L1/L2).  The 64 lanes' partial
-// sums are reduced by a transposing butterfly (each step halves the values a
-// lane carries), the 32 x MP results meet in LDS, and wavefront 0 runs the
-// same epilogue as the tiled kernel.
+// Workgroup = 8 wavefronts; wavefront w streams R consecutive packed weight
+// rows with 16-byte coalesced loads, every lane covering a slice of K for
+// all MP activation rows (read through L1/L2).  R = 4 (32 rows: a 16-row
+// pair group) for the gated and rotary epilogues, R = 1 (8 rows, four times
+// the workgroups) for the others.  The 64 lanes' partial sums are reduced by
+// a transposing butterfly (each step halves the values a lane carries), the
+// results meet in LDS, and wavefront 0 runs the same epilogue as the tiled
+// kernel.
 template <int NV>
 __device__ __forceinline__ float lane_transpose_sum(float (&v)[NV], int lane, int& index) {
   index = 0;
@@ -793,13 +814,13 @@ __device__ __forceinline__ float lane_transpose_sum(float (&v)[NV], int lane, in
   return v[0];
 }
 
-template <typename T, int MP>
+template <typename T, int MP, int R>
 __global__ __launch_bounds__(512) void k_gemm_skinny(GemmArgs a) {
   constexpr int VN = 16 / static_cast<int>(sizeof(T));
-  constexpr int R = 4;
+  constexpr int ROWS = 8 * R;               // weight rows per workgroup
   typedef typename std::conditional<sizeof(T) == 4, f32x4v, u32x4>::type V;
-  __shared__ float res[32][MP + 1];
-  const int n0 = blockIdx.x * 32;
+  __shared__ float res[ROWS][MP + 1];
+  const int n0 = blockIdx.x * ROWS;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const T* W = static_cast<const T*>(a.W);
   const T* A = static_cast<const T*>(a.A);
@@ -845,27 +866,140 @@ __global__ __launch_bounds__(512) void k_gemm_skinny(GemmArgs a) {
   __syncthreads();
   if (wave != 0) return;
   SiteMax sm;
-  const int m = lane >> 2, q = lane & 3;
-  if (m < MP && m < a.M) {
-    float va[4], vb[4];
+  if (R == 4) {
+    // a 16-row pair group: packed rows n0 + 4q + r and n0 + 16 + 4q + r
+    const int m = lane >> 2, q = lane & 3;
+    if (m < MP && m < a.M) {
+      float va[4], vb[4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      va[r] = res[4 * q + r][m];
-      vb[r] = res[16 + 4 * q + r][m];
+      for (int r = 0; r < 4; ++r) {
+        va[r] = res[4 * q + r][m];
+        vb[r] = res[16 + 4 * q + r][m];
+      }
+      epi_pair<T>(a, m, n0 + 4 * q, va, vb, sm);
     }
-    epi_pair<T>(a, m, n0 + 4 * q, va, vb, sm);
+  } else {
+    // independent columns: 8 rows as two groups of 4; the partner columns
+    // the pair epilogue would also write lie beyond this workgroup's N
+    GemmArgs b = a;
+    b.N = a.N - n0 < ROWS ? a.N : n0 + ROWS;
+    const int m = lane >> 1, q = lane & 1;
+    if (m < MP && m < a.M) {
+      float va[4], vb[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int r = 0; r < 4; ++r) va[r] = res[4 * q + r][m];
+      epi_pair<T>(b, m, n0 + 4 * q, va, vb, sm);
+    }
+  }
+  site_flush(a, sm);
+}
+
+// Independent-column epilogues on a narrow output: workgroup = 8 weight
+// rows, and the 8 wavefronts split K instead of the rows, each covering all
+// 8 rows for its K slice, so every lane's loads (8 weight and MP activation
+// vectors per step) leave together and a short K needs a single round trip
+// to memory.  Lane partials are reduced by the transposing butterfly, the 8
+// wavefronts' sums are added in LDS.
+template <typename T, int MP>
+__global__ __launch_bounds__(512) void k_gemm_skinny_ks(GemmArgs a) {
+  constexpr int VN = 16 / static_cast<int>(sizeof(T));
+  constexpr int R = 8;
+  typedef typename std::conditional<sizeof(T) == 4, f32x4v, u32x4>::type V;
+  __shared__ float part[8][R * MP];
+  __shared__ float res[R][MP + 1];
+  const int n0 = blockIdx.x * R;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const T* W = static_cast<const T*>(a.W);
+  const T* A = static_cast<const T*>(a.A);
+  // this wavefront's K slice, a multiple of VN
+  const int per = ((a.K + 8 * VN - 1) / (8 * VN)) * VN;
+  const int kb = wave * per, ke = min(a.K, kb + per);
+  const T* wrow[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    int n = n0 + r;
+    n = n < a.N ? n : a.N - 1;
+    wrow[r] = W + static_cast<long long>(n) * a.ldw;
+  }
+  const T* arow[MP];
+#pragma unroll
+  for (int m = 0; m < MP; ++m) arow[m] = A + static_cast<long long>(m < a.M ? m : a.M - 1) * a.lda;
+  float acc[R * MP];
+#pragma unroll
+  for (int j = 0; j < R * MP; ++j) acc[j] = 0.f;
+  for (int k = kb + lane * VN; k < ke; k += 64 * VN) {
+    V wv[R], av[MP];
+#pragma unroll
+    for (int r = 0; r < R; ++r) wv[r] = *reinterpret_cast<const V*>(wrow[r] + k);
+#pragma unroll
+    for (int m = 0; m < MP; ++m) av[m] = *reinterpret_cast<const V*>(arow[m] + k);
+#pragma unroll
+    for (int m = 0; m < MP; ++m) {
+      const T* ae = reinterpret_cast<const T*>(&av[m]);
+#pragma unroll
+      for (int i = 0; i < VN; ++i) {
+        const float x = to_f32(ae[i]);
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+          acc[r * MP + m] = fmaf(to_f32(reinterpret_cast<const T*>(&wv[r])[i]), x, acc[r * MP + m]);
+      }
+    }
+  }
+  int idx;
+  const float sum = lane_transpose_sum<R * MP>(acc, lane, idx);
+  if ((lane & (64 / (R * MP) - 1)) == 0) part[wave][idx] = sum;
+  __syncthreads();
+  if (threadIdx.x < R * MP) {
+    float t = 0.f;
+#pragma unroll
+    for (int w2 = 0; w2 < 8; ++w2) t += part[w2][threadIdx.x];
+    res[threadIdx.x / MP][threadIdx.x % MP] = t;
+  }
+  __syncthreads();
+  if (wave != 0) return;
+  SiteMax sm;
+  GemmArgs b = a;
+  b.N = a.N - n0 < R ? a.N : n0 + R;
+  const int m = lane >> 1, q = lane & 1;
+  if (m < MP && m < a.M) {
+    float va[4], vb[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int r = 0; r < 4; ++r) va[r] = res[4 * q + r][m];
+    epi_pair<T>(b, m, n0 + 4 * q, va, vb, sm);
   }
   site_flush(a, sm);
 }
 
 template <typename T>
+static void skinny_ks(const GemmArgs& a, hipStream_t s) {
+  const dim3 grid((a.N + 7) / 8), block(512);
+  if (a.M <= 1) hipLaunchKernelGGL((k_gemm_skinny_ks<T, 1>), grid, block, 0, s, a);
+  else if (a.M <= 2) hipLaunchKernelGGL((k_gemm_skinny_ks<T, 2>), grid, block, 0, s, a);
+  else if (a.M <= 4) hipLaunchKernelGGL((k_gemm_skinny_ks<T, 4>), grid, block, 0, s, a);
+  else hipLaunchKernelGGL((k_gemm_skinny_ks<T, 8>), grid, block, 0, s, a);
+}
+
+template <typename T, int R>
+static void skinny_r(const GemmArgs& a, hipStream_t s) {
+  const dim3 grid((a.N + 8 * R - 1) / (8 * R)), block(512);
+  if (a.M <= 1) hipLaunchKernelGGL((k_gemm_skinny<T, 1, R>), grid, block, 0, s, a);
+  else if (a.M <= 2) hipLaunchKernelGGL((k_gemm_skinny<T, 2, R>), grid, block, 0, s, a);
+  else if (a.M <= 4) hipLaunchKernelGGL((k_gemm_skinny<T, 4, R>), grid, block, 0, s, a);
+  else if (a.M <= 8) hipLaunchKernelGGL((k_gemm_skinny<T, 8, R>), grid, block, 0, s, a);
+  else hipLaunchKernelGGL((k_gemm_skinny<T, 16, R>), grid, block, 0, s, a);
+}
+
+template <typename T>
 static void skinny_t(const GemmArgs& a, hipStream_t s) {
-  const dim3 grid((a.N + 31) / 32), block(512);
-  if (a.M <= 1) hipLaunchKernelGGL((k_gemm_skinny<T, 1>), grid, block, 0, s, a);
-  else if (a.M <= 2) hipLaunchKernelGGL((k_gemm_skinny<T, 2>), grid, block, 0, s, a);
-  else if (a.M <= 4) hipLaunchKernelGGL((k_gemm_skinny<T, 4>), grid, block, 0, s, a);
-  else if (a.M <= 8) hipLaunchKernelGGL((k_gemm_skinny<T, 8>), grid, block, 0, s, a);
-  else hipLaunchKernelGGL((k_gemm_skinny<T, 16>), grid, block, 0, s, a);
+  // the gated and rotary epilogues combine packed rows 16 apart; a wide
+  // output (the head) has workgroups enough with 32 rows each, and four rows
+  // per wavefront reuse every activation load four times
+  if (a.epi == kEpiGatedGelu || a.epi == kEpiGatedSilu || a.epi == kEpiRope || a.N >= 8192)
+    skinny_r<T, 4>(a, s);
+  else if (a.M <= 8 && a.N < 2048)     // few row groups: split K across the wavefronts
+    skinny_ks<T>(a, s);
+  else
+    skinny_r<T, 1>(a, s);
 }
 
 static bool g_force_simple = false;

@@ -34,6 +34,11 @@ struct GemmArgs {
   int seq;                  // positions are m % seq, or pos[m] when pos is set
   const int32_t* pos;       // per-row positions (decode step), or null
   int head_dim; int d_model;
+  // decode step, QKV projection only (kc != null): the k and v columns of
+  // row b are also stored at position pos[b] of the KV cache
+  // ([B][H][kv_max_seq][head_dim]) and the position marked valid, unless the
+  // step trapped
+  void* kc; void* vc; uint8_t* kv_valid; int kv_max_seq; int heads;
 };
 // M <= 16 rows (a decode step, or a tiny forward) runs on a weight-streaming
 // kernel; larger M on the tiled MFMA kernel.
@@ -109,7 +114,7 @@ struct DecAttnArgs {
   const int32_t* pos;       // keys 0 .. pos[b] of sequence b
   void* ctx;                // [B, d]
   float* part;              // [B*H*nsplit*(hd+2)] partial softmax state per key chunk
-  int nsplit, chunk;
+  int nsplit, chunk;        // key chunks per head (1: no merge pass) and their size
   float scale;
 };
 void launch_decode_attention(const DecAttnArgs& a, hipStream_t s);

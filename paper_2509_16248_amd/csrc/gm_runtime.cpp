@@ -102,7 +102,7 @@ struct gm_model {
   uint8_t* kv_valid = nullptr;
   int32_t *seqlen = nullptr, *dpos = nullptr;
   float* dpart = nullptr;
-  int dec_nsplit = 0, dec_chunk = 0;
+  int dec_nsplit = 0;
   int cache_B = 0;          // batch of the last prefill (host-side), 0 = none
 
   int alloc(void** p, size_t bytes) {
@@ -354,6 +354,14 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
   auto gemm = [&](int kind, const void* A, int K, const void* W, int N, int epi, const void* bias,
                   void* out, int ldo, const void* resid, int site) {
     GemmArgs q = ga;
+    if (dec && kind == GM_K_GEMM_QKV) {
+      // a decode step stores this layer's new k and v from the epilogue
+      q.kc = m->kc[cur_layer];
+      q.vc = m->vc[cur_layer];
+      q.kv_valid = m->kv_valid;
+      q.kv_max_seq = c.max_seq;
+      q.heads = c.n_heads;
+    }
     q.A = A;
     q.lda = K;
     q.K = K;
@@ -421,12 +429,21 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
   da.pos = m->dpos;
   da.ctx = m->ctx;
   da.part = m->dpart;
-  da.nsplit = m->dec_nsplit;
-  da.chunk = m->dec_chunk;
+  {
+    // split the keys only when there are fewer than ~100 (sequence, head)
+    // pairs to spread over the GPU (a split costs a merge launch); chunks
+    // are a multiple of 64 keys
+    int want = (96 + B * c.n_heads - 1) / (B * c.n_heads);
+    want = want < m->dec_nsplit ? want : m->dec_nsplit;
+    want = want > 1 ? want : 1;
+    da.chunk = 64 * ((c.max_seq + 64 * want - 1) / (64 * want));
+    da.nsplit = (c.max_seq + da.chunk - 1) / da.chunk;
+  }
   da.scale = at.scale;
   auto attention = [&]() {
-    if (c.kv_cache) {
-      // this layer's k and v go to the cache (prefill: every position; decode: pos[b])
+    if (c.kv_cache && !dec) {
+      // this layer's k and v go to the cache (a decode step stores them from
+      // the QKV epilogue)
       kv.kc = m->kc[cur_layer];
       kv.vc = m->vc[cur_layer];
       if (on()) launch_kv_store(kv, s);
@@ -669,9 +686,8 @@ int gm_model_create(const gm_config* cfg, const gm_weights* w, gm_model** out) {
     for (int l = 0; l < c.n_layers; ++l)
       if ((rc = m->alloc(&m->kc[l], per_layer)) || (rc = m->alloc(&m->vc[l], per_layer)))
         return fail(rc);
-    // keys per split chunk: a multiple of 64, at most 32 chunks
-    m->dec_chunk = 64 * ((c.max_seq + 64 * 32 - 1) / (64 * 32));
-    m->dec_nsplit = (c.max_seq + m->dec_chunk - 1) / m->dec_chunk;
+    // at most 32 key chunks per head (the workspace bound)
+    m->dec_nsplit = 32;
     void* q = nullptr;
     if ((rc = m->alloc(&q, static_cast<size_t>(c.max_batch) * c.max_seq))) return fail(rc);
     m->kv_valid = static_cast<uint8_t*>(q);
