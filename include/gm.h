@@ -57,13 +57,16 @@ enum { GM_POS_NONE = 0, GM_POS_LEARNED = 1, GM_POS_ROTARY = 2 };
 
 /* Trap codes, in the order the guards run (smaller code = earlier guard). */
 enum { GM_TRAP_NONE = 0, GM_TRAP_TOKEN_RANGE = 1, GM_TRAP_MASK_VALUE = 2,
-       GM_TRAP_ROPE_CAPACITY = 3, GM_TRAP_KV_CAPACITY = 4 };
+       GM_TRAP_ROPE_CAPACITY = 3, GM_TRAP_KV_CAPACITY = 4, GM_TRAP_MASK_GUARD = 5 };
 
 /* Execution modes (gm_set_exec_mode). */
 enum { GM_EXEC_GRAPH = 0, GM_EXEC_EAGER = 1, GM_EXEC_FRAGMENTED = 2 };
 
 /* Kinds of deferred effect records (rule [Defer]). */
-enum { GM_EFFECT_PAD = 1, GM_EFFECT_REGROW = 2, GM_EFFECT_CLAMP = 3 };
+enum { GM_EFFECT_PAD = 1, GM_EFFECT_REGROW = 2, GM_EFFECT_CLAMP = 3, GM_EFFECT_LOG = 4 };
+
+/* Rotary frequency scaling (gm_config.rope_scaling). */
+enum { GM_ROPE_PLAIN = 0, GM_ROPE_LONG_SHORT = 1 };
 
 /* ------------------------------------------------------------ config
  * Model hyper-parameters.  Read only during gm_model_create.
@@ -79,9 +82,19 @@ enum { GM_EFFECT_PAD = 1, GM_EFFECT_REGROW = 2, GM_EFFECT_CLAMP = 3 };
  *  cached length) grows it on the device to exactly that length.
  *  fp16_clamp (f16 + PRE only): after each residual add, if no element is
  *  NaN and max |h| > 65504 - clamp_margin, h is clamped to that bound.
- *  kv_cache (causal models without fp16_clamp): keep every layer's k and v
- *  for max_batch x max_seq positions so that gm_decode_step can extend the
- *  sequences of the last forward one token at a time.
+ *  kv_cache (causal models without fp16_clamp or rope_scaling): keep every
+ *  layer's k and v for max_batch x max_seq positions so that gm_decode_step
+ *  can extend the sequences of the last forward one token at a time.
+ *  log_hidden: after every layer, record max |h| of each sequence (a [B]
+ *  tensor) as a deferred log effect (GM_EFFECT_LOG) replayed after the
+ *  forward (rule [Defer] with a tensor argument).
+ *  rope_scaling GM_ROPE_LONG_SHORT (rotary only): two frequency sets,
+ *  theta_i = 1 / (factor_i * base^(2i/hd)) with the short or the long
+ *  factors (gm_weights.rope_short_factor / rope_long_factor, fp32 [hd/2]);
+ *  a forward uses the long set when max(position) + 1 > rope_orig_max
+ *  (rule [Where]: both tables are built at create, a device flag selects);
+ *  cos and sin are scaled by rope_attn_factor.  The regrow predicate does
+ *  not apply: both tables hold rope_capacity rows from the start.
  */
 typedef struct gm_config {
   int32_t abi_version;      /* must be GM_ABI_VERSION */
@@ -95,6 +108,10 @@ typedef struct gm_config {
   int32_t fp16_clamp;
   float   clamp_margin;
   int32_t kv_cache;
+  int32_t log_hidden;
+  int32_t rope_scaling;
+  int32_t rope_orig_max;
+  float   rope_attn_factor;
 } gm_config;
 
 /* ------------------------------------------------------------ weights
@@ -118,6 +135,7 @@ typedef struct gm_layer_weights {
 typedef struct gm_weights {
   const void *tok_emb, *pos_emb, *emb_ln_g, *emb_ln_b, *lnf_g, *lnf_b, *lm_head;
   const gm_layer_weights *layers;   /* host array of n_layers entries */
+  const float *rope_short_factor, *rope_long_factor;   /* device fp32 [hd/2], rope_scaling only */
 } gm_weights;
 
 typedef struct gm_model gm_model;
@@ -133,15 +151,19 @@ typedef struct gm_decisions {
   float   clamp_absmax[2 * GM_MAX_LAYERS]; /* max |h| over non-NaN elements */
   int32_t clamp_nan[2 * GM_MAX_LAYERS];    /* some element of h was NaN     */
   int32_t forward_index;  /* 0-based count of forwards enqueued before it     */
+  int32_t rope_long;      /* rope_scaling: the long frequency set was used    */
 } gm_decisions;
 
 /* One deferred effect: what the original program would have printed. */
 typedef struct gm_effect {
-  int32_t forward;   /* forward_index of the forward that recorded it */
-  int32_t kind;      /* GM_EFFECT_*                                   */
-  int32_t layer;     /* clamp: layer; otherwise -1                    */
-  int32_t site;      /* clamp: 0 attention, 1 FFN; otherwise -1       */
-  float   value;     /* pad: #pad positions; regrow: need; clamp: max |h| */
+  int32_t forward;   /* forward_index of the forward that recorded it          */
+  int32_t kind;      /* GM_EFFECT_*                                            */
+  int32_t layer;     /* clamp, log: layer; otherwise -1                        */
+  int32_t site;      /* clamp: 0 attention, 1 FFN; log: 0; otherwise -1        */
+  float   value;     /* pad: #pad positions; regrow: need; clamp: max |h|;
+                        log: number of values                                  */
+  int32_t n_values;  /* log: B (max |h| of each sequence); otherwise 0        */
+  const float *values; /* host memory valid during the callback, or NULL      */
 } gm_effect;
 
 typedef void (*gm_effect_cb)(const gm_effect *effect, void *user);
@@ -150,7 +172,7 @@ typedef void (*gm_effect_cb)(const gm_effect *effect, void *user);
 enum { GM_K_PROLOGUE = 0, GM_K_ROPE = 1, GM_K_EMBED = 2, GM_K_NORM = 3,
        GM_K_GEMM_QKV = 4, GM_K_ATTENTION = 5, GM_K_GEMM_O = 6, GM_K_GEMM_UP = 7,
        GM_K_GEMM_DOWN = 8, GM_K_GEMM_HEAD = 9, GM_K_EFFECTS = 10, GM_K_KV_STORE = 11,
-       GM_K_ARGMAX = 12 };
+       GM_K_ARGMAX = 12, GM_K_LOG = 13 };
 
 /* One kernel launch of a profiled forward.  flops/bytes are the launch's
  * algorithmic work (2*M*N*K for a GEMM; 4*hd*visible (query,key) pairs per
@@ -264,6 +286,21 @@ int gm_read_decisions(gm_model *m, gm_decisions *out, hipStream_t stream);
 /* Device address of the model's int32 decision slots, for zero-sync reads by
  * later kernels: [0] pad_any, [1] regrow, [2] need, [3] cached_len. */
 const int32_t *gm_decisions_device_ptr(const gm_model *m);
+
+/* Validation guard `if not torch.equal(attn_mask, expected): raise
+ * ValueError("unsupported attention mask")` on every later forward, lowered
+ * as in rule [Trap]: the host checks the metadata (expected is int32 [B, S];
+ * a forward of another shape fails the guard), the device checks
+ * (attn_mask == expected).all() and sets trap GM_TRAP_MASK_GUARD at the
+ * first differing element.  expected: device, 16-byte aligned, valid while
+ * the guard is set; NULL removes the guard.  Synchronises the device and
+ * drops the cached graphs (they hold the previous guard). */
+int gm_set_mask_guard(gm_model *m, const int32_t *expected, int32_t B, int32_t S);
+
+/* The original exception of a trap code ("uid" of rule [Trap]): its Python
+ * type name and message, for the caller to raise when gm_check_error
+ * reports the code.  Static strings. */
+int gm_trap_info(int32_t code, const char **exception_type, const char **message);
 
 /* Return and clear the sticky trap word: *code = GM_TRAP_* of the first
  * failing guard of the first trapped forward since the last call, *index =

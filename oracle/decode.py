@@ -32,10 +32,8 @@ from typing import List, Optional
 
 import numpy as np
 
-from .model import (EFFECT_PAD, EFFECT_REGROW, TRAP_ROPE_CAPACITY, TRAP_TOKEN_RANGE, Effect,
-                    OracleModel, Trap)
-
-TRAP_KV_CAPACITY = 4
+from .model import (EFFECT_PAD, EFFECT_REGROW, TRAP_KV_CAPACITY, TRAP_ROPE_CAPACITY,
+                    TRAP_TOKEN_RANGE, Effect, OracleModel, Trap)
 
 
 def greedy(logits_row: np.ndarray) -> int:

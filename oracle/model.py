@@ -45,11 +45,24 @@ from . import numerics as nx
 TRAP_TOKEN_RANGE = 1
 TRAP_MASK_VALUE = 2
 TRAP_ROPE_CAPACITY = 3
+TRAP_KV_CAPACITY = 4
+TRAP_MASK_GUARD = 5
+
+# The exception each guard of the original program raises (type, message):
+# what a [Trap] failure is reported as once it surfaces on the host.
+TRAP_INFO = {
+    TRAP_TOKEN_RANGE: ("IndexError", "token id out of range"),
+    TRAP_MASK_VALUE: ("ValueError", "attention mask values must be 0 or 1"),
+    TRAP_ROPE_CAPACITY: ("ValueError", "rotary position exceeds the table capacity"),
+    TRAP_KV_CAPACITY: ("IndexError", "sequence exceeds the KV cache capacity"),
+    TRAP_MASK_GUARD: ("ValueError", "unsupported attention mask"),
+}
 
 # Kinds of deferred effect records.
 EFFECT_PAD = 1
 EFFECT_REGROW = 2
 EFFECT_CLAMP = 3
+EFFECT_LOG = 4
 
 FP16_MAX = 65504.0
 
@@ -71,6 +84,7 @@ class Effect:
     layer: int
     site: int
     value: float
+    values: Optional[Tuple[float, ...]] = None   # tensor argument of a log, as cloned
 
 
 @dataclasses.dataclass
@@ -86,6 +100,7 @@ class OracleResult:
     clamp_nan: List[Tuple[bool, bool]]
     clamp_margin: List[Tuple[float, float]]   # distance of max |pre-rounding| from the trip boundary
     effects: List[Effect]
+    rope_long: bool = False          # long/short rotary select: long factors used
 
 
 def _cfg_get(cfg, name):
@@ -108,7 +123,9 @@ class OracleModel:
         self.forward_count = 0
         self.cached_len = 0
         self.rope_cos = self.rope_sin = None
-        if cfg.pos == "rotary":
+        # `if not torch.equal(attention_mask, expected): raise` when set
+        self.mask_guard: Optional[np.ndarray] = None
+        if cfg.pos == "rotary" and cfg.rope_scaling == "none":
             self._rope_build(cfg.rope_init_len)
 
     # ---------------------------------------------------------------- helpers
@@ -184,9 +201,29 @@ class OracleModel:
         positions = np.broadcast_to(np.arange(S), (B, S))
         need = int(positions.max()) + 1
         regrow = False
-        if c.pos == "rotary":
-            if need > c.rope_capacity:
-                raise Trap(TRAP_ROPE_CAPACITY, 0)
+        rope_long = False
+        if c.pos == "rotary" and need > c.rope_capacity:
+            raise Trap(TRAP_ROPE_CAPACITY, 0)
+
+        # --- validation guard `if not torch.equal(mask, expected): raise`
+        # (shapes and dtypes first: torch.equal is False when they differ).
+        if self.mask_guard is not None:
+            exp = np.asarray(self.mask_guard)
+            if exp.shape != mask.shape or exp.dtype != mask.dtype:
+                raise Trap(TRAP_MASK_GUARD, 0)
+            diff = (mask != exp).reshape(-1)
+            if diff.any():
+                raise Trap(TRAP_MASK_GUARD, int(np.argmax(diff)))
+
+        if c.pos == "rotary" and c.rope_scaling == "long_short":
+            # Phi-4-style select: the long factors once the sequence exceeds
+            # the original context; cos/sin built from the chosen factors
+            rope_long = need > c.rope_orig_max
+            factor = self.w.globals["rope_long_factor" if rope_long else "rope_short_factor"]
+            self.rope_cos, self.rope_sin = nx.rope_table_scaled(
+                S, c.head_dim, c.rope_base, factor, c.rope_attn_factor)
+            self.cached_len = c.rope_capacity
+        elif c.pos == "rotary":
             regrow = need > self.cached_len
             if "regrow" in force:
                 regrow = bool(force["regrow"])
@@ -200,10 +237,10 @@ class OracleModel:
 
         if rows is None:
             rows = list(range(B))
-        if c.fp16_clamp and len(rows) != B:
-            raise ValueError("the clamp predicate needs every sequence")
+        if (c.fp16_clamp or c.log_hidden) and len(rows) != B:
+            raise ValueError("the clamp predicate and the hidden log read every sequence")
         if prefix is not None:
-            if not c.causal or c.fp16_clamp:
+            if not c.causal or c.fp16_clamp or c.log_hidden:
                 raise ValueError("a prefix equals the full forward only for causal models")
             S = min(S, prefix)
         ids_r = ids[rows][:, :S]
@@ -279,6 +316,11 @@ class OracleModel:
                 h = self.R(self._norm(h, W["ln2_g"], W.get("ln2_b")))
             h, info = self._clamp_site(h, pre, l, 1, force, fwd, effects)
             site_out.append(info)
+            if c.log_hidden:
+                # logger.info(..., h.abs().amax per sequence): the tensor is
+                # taken here; the original prints it at once
+                vals = tuple(float(v) for v in np.abs(h).reshape(Br, -1).max(axis=1))
+                effects.append(Effect(fwd, EFFECT_LOG, l, 0, float(Br), vals))
             clamp.append((site_out[0][0], site_out[1][0]))
             absmaxes.append((site_out[0][1], site_out[1][1]))
             nans.append((site_out[0][2], site_out[1][2]))
@@ -296,7 +338,7 @@ class OracleModel:
             logits=nx.to_storage(logits, self.dt), logits_f64=logits,
             pad_any=pad_any, regrow=regrow, need=need,
             cached_len=self.cached_len, clamp=clamp, clamp_absmax=absmaxes,
-            clamp_nan=nans, clamp_margin=margins, effects=effects)
+            clamp_nan=nans, clamp_margin=margins, effects=effects, rope_long=rope_long)
 
     def _clamp_site(self, h, pre, l, s, force, fwd, effects):
         """fp16 overflow guard after a residual add: ``if abs(h).max() >

@@ -127,6 +127,28 @@ def rope_table(n_pos: int, head_dim: int, base: float):
             np.sin(ang).astype(np.float32).astype(np.float64))
 
 
+def rope_table_scaled(n_pos: int, head_dim: int, base: float, factor: np.ndarray,
+                      attn: float):
+    """cos/sin tables [n_pos, head_dim/2] of a scaled rotary frequency set
+    (the long/short factors of a long-context rope).
+
+    theta_i = 1 / (factor_i * base ** (2 i / head_dim)), with the power
+    rounded to float32 and the product and the quotient as float32
+    operations (the frequency buffer is float32); angle = p * theta_i in
+    float64; cos and sin rounded to float32 and multiplied by ``attn`` as a
+    float32 product."""
+    half = head_dim // 2
+    i = np.arange(half, dtype=np.float64)
+    ib = (base ** (2.0 * i / head_dim)).astype(np.float32)
+    denom = (np.asarray(factor, dtype=np.float32) * ib).astype(np.float32)
+    theta = (np.float32(1.0) / denom).astype(np.float32).astype(np.float64)
+    ang = np.arange(n_pos, dtype=np.float64)[:, None] * theta[None, :]
+    a = np.float32(attn)
+    c = (np.cos(ang).astype(np.float32) * a).astype(np.float32)
+    s = (np.sin(ang).astype(np.float32) * a).astype(np.float32)
+    return c.astype(np.float64), s.astype(np.float64)
+
+
 def apply_rope(x: np.ndarray, cos: np.ndarray, sin: np.ndarray) -> np.ndarray:
     """Rotate-half rotary embedding on the last axis (pairs i, i + hd/2).
     ``x`` is [..., S, hd]; ``cos``/``sin`` are [S, hd/2]."""

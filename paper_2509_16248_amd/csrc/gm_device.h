@@ -24,6 +24,9 @@ enum Slot : int {
   kFifoDropped = 10, // persistent until flush: records lost to overflow
   kPadCount = 11,    // per-forward: number of mask zeros
   kFwdIndex = 12,    // per-forward: index of this forward
+  kLogCount = 13,    // persistent until flush: log values written to the arena
+  kLogDropped = 14,  // persistent until flush: log values lost to overflow
+  kRopeLong = 15,    // per-forward: long rotary frequencies selected
   kClampBase = 16,                    // per-forward: 2*kMaxLayers trip decisions
   kAbsmaxBase = kClampBase + 128,     // per-forward: bits of max |h| per site
   kNanBase = kAbsmaxBase + 128,       // per-forward: NaN seen per site
@@ -32,9 +35,10 @@ enum Slot : int {
 constexpr int kMaxLayers = 64;
 constexpr uint32_t kTrapNone = 0xFFFFFFFFu;
 
-struct EffectRec {   // mirrors gm_effect
+struct EffectRec {   // gm_effect, with its tensor payload as a range of the log arena
   int32_t forward, kind, layer, site;
   float value;
+  int32_t offset, count;
 };
 
 // ------------------------------------------------------------ vector types

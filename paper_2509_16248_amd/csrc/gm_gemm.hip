@@ -124,8 +124,10 @@ __device__ __forceinline__ void epi_pair(const GemmArgs& a, int m, int nA,
     const int i = (within >> 5) * 16 + (within & 15);
     int pos = a.pos ? a.pos[m] : m % a.seq;
     pos = pos < a.rope_rows ? pos : a.rope_rows - 1;
-    const float* cs = a.rope_cos + static_cast<long long>(pos) * P + i;
-    const float* sn = a.rope_sin + static_cast<long long>(pos) * P + i;
+    // [Where]: both frequency sets exist; the forward's flag selects one
+    const long long set = a.rope_set_stride && a.state[kRopeLong] ? a.rope_set_stride : 0;
+    const float* cs = a.rope_cos + set + static_cast<long long>(pos) * P + i;
+    const float* sn = a.rope_sin + set + static_cast<long long>(pos) * P + i;
     float o1[4], o2[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {

@@ -31,6 +31,8 @@ struct GemmArgs {
   const void* resid; int ldr;
   int32_t* state; int site; // clamp-site reduction target (site < 0: none)
   const float* rope_cos; const float* rope_sin; int rope_rows;
+  int rope_set_stride;      // long/short select: the long set starts this many
+                            // floats later, used when state[kRopeLong]
   int seq;                  // positions are m % seq, or pos[m] when pos is set
   const int32_t* pos;       // per-row positions (decode step), or null
   int head_dim; int d_model;
@@ -56,12 +58,31 @@ struct AttnArgs {
 };
 void launch_attention(const AttnArgs& a, hipStream_t s);
 
+// The forward's guards and predicates (see k_prologue).  expected != null
+// adds the mask-equality guard (trap 5): guard_meta_ok is the host's shape
+// check of expected against [B, S].  log_vals > 0 zeroes that many floats of
+// log_stage (per-forward tensor log values).  rope_orig > 0: long/short
+// rotary frequency select, long when max(position) + 1 > rope_orig.
 void launch_prologue(const int32_t* ids, const int32_t* mask, int B, int S,
                      int vocab, int rotary, int capacity, int n_sites,
+                     const int32_t* expected, int guard_meta_ok,
+                     float* log_stage, int log_vals, int rope_orig,
                      int32_t* state, hipStream_t s);
+
+// Tensor-valued log at layer `layer`: stage[layer*B + b] = max |x| over the
+// rows of sequence b of x [B*S, d] (NaN if any element is NaN), as float bits
+// reduced with integer max.  stage must be zero before the first call.
+// clamp_site >= 0: that site's clamp select, if it tripped, applies to x.
+void launch_log_seqmax(const void* x, int dtype, int B, int S, int d, float* stage, int layer,
+                       const int32_t* state, int clamp_site, float clamp_thr, hipStream_t s);
 
 void launch_rope_fill(float* cos, float* sin, int head_dim, double base,
                       const int32_t* state, hipStream_t s);
+
+// Rows [0, rows) of a frequency set scaled by factor[hd/2] (device fp32),
+// cos/sin multiplied by attn.
+void launch_rope_fill_scaled(float* cos, float* sin, int head_dim, double base,
+                             const float* factor, float attn, int rows, hipStream_t s);
 
 struct RowArgs {
   int dtype;
@@ -77,8 +98,12 @@ struct RowArgs {
 };
 void launch_rownorm(const RowArgs& a, hipStream_t s);
 
+// Effects of a forward in program order: pad, regrow, then per layer the two
+// clamp sites and (n_log_layers > 0) the layer's tensor log of B values,
+// copied from log_stage into the arena (the value at the call site).
 void launch_emit_effects(int32_t* state, void* fifo, int fifo_cap, int n_sites,
-                         hipStream_t s);
+                         const float* log_stage, float* arena, int arena_cap, int n_log_layers,
+                         int B, hipStream_t s);
 
 // ------------------------------------------------------------ decode step
 // KV cache: per layer, K and V as [max_batch][H][max_seq][hd] (act dtype) and

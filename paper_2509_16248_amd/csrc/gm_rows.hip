@@ -27,6 +27,8 @@ constexpr int kPrologueThreads = 1024;
 __global__ __launch_bounds__(kPrologueThreads) void k_prologue(
     const int32_t* __restrict__ ids, const int32_t* __restrict__ mask, int B,
     int S, int vocab, int rotary, int capacity, int n_sites,
+    const int32_t* __restrict__ expected, int guard_meta_ok,
+    float* __restrict__ log_stage, int log_vals, int rope_orig,
     int32_t* __restrict__ state) {
   __shared__ int kv[1024];
   __shared__ uint32_t red_trap[kPrologueThreads / 64];
@@ -39,6 +41,7 @@ __global__ __launch_bounds__(kPrologueThreads) void k_prologue(
     state[kAbsmaxBase + i] = 0;
     state[kNanBase + i] = 0;
   }
+  for (int i = tid; i < log_vals; i += blockDim.x) log_stage[i] = 0.f;
   __syncthreads();
   uint32_t trap = kTrapNone;
   int pads = 0, need = 0;
@@ -49,6 +52,9 @@ __global__ __launch_bounds__(kPrologueThreads) void k_prologue(
     const int s = i % S;
     if (id < 0 || id >= vocab) trap = min(trap, (1u << 24) | static_cast<uint32_t>(i));
     if (mk != 0 && mk != 1) trap = min(trap, (2u << 24) | static_cast<uint32_t>(i));
+    // `if not torch.equal(mask, expected): raise` as (mask == expected).all()
+    if (expected && guard_meta_ok && mk != expected[i])
+      trap = min(trap, (5u << 24) | static_cast<uint32_t>(i));
     if (mk == 0) ++pads;
     else atomicMax(&kv[i / S], s + 1);
     need = max(need, s + 1);           // positions are 0..S-1
@@ -75,10 +81,12 @@ __global__ __launch_bounds__(kPrologueThreads) void k_prologue(
       need = max(need, red_need[i]);
     }
     if (rotary && need > capacity) trap = min(trap, 3u << 24);
+    if (expected && !guard_meta_ok) trap = min(trap, 5u << 24);   // shapes differ: never equal
     int regrow = 0;
     const int cached = state[kCachedLen];
     int from = 0, to = 0;
-    if (rotary && trap == kTrapNone && need > cached) {
+    state[kRopeLong] = rope_orig > 0 && need > rope_orig;
+    if (rotary && rope_orig <= 0 && trap == kTrapNone && need > cached) {
       regrow = 1;
       from = cached;
       to = need;
@@ -99,9 +107,59 @@ __global__ __launch_bounds__(kPrologueThreads) void k_prologue(
 
 void launch_prologue(const int32_t* ids, const int32_t* mask, int B, int S,
                      int vocab, int rotary, int capacity, int n_sites,
+                     const int32_t* expected, int guard_meta_ok,
+                     float* log_stage, int log_vals, int rope_orig,
                      int32_t* state, hipStream_t s) {
   hipLaunchKernelGGL(k_prologue, dim3(1), dim3(kPrologueThreads), 0, s, ids,
-                     mask, B, S, vocab, rotary, capacity, n_sites, state);
+                     mask, B, S, vocab, rotary, capacity, n_sites, expected, guard_meta_ok,
+                     log_stage, log_vals, rope_orig, state);
+}
+
+// ------------------------------------------------------------ tensor log
+// max |x| per sequence for the deferred log of a layer ([Defer] with a tensor
+// argument: the value is taken here, at the call site, and replayed after
+// the forward).  Absolute values as float bits compare like integers, and a
+// NaN's bits exceed every number's, so an integer max propagates NaN.
+// A clamp site whose select is still pending (applied by the next reader of
+// h) is applied here too: the log sees h as the program holds it.
+template <typename T>
+__global__ __launch_bounds__(256) void k_log_seqmax(const T* __restrict__ x, int S, int d,
+                                                     float* __restrict__ stage,
+                                                     const int32_t* __restrict__ state,
+                                                     int site, float thr) {
+  const int b = blockIdx.y;
+  const long long n = static_cast<long long>(S) * d;
+  const T* xs = x + static_cast<long long>(b) * n;
+  const bool trip = site >= 0 && clamp_trip(state, site, thr);
+  uint32_t mx = 0;
+  for (long long i = blockIdx.x * 256ll + threadIdx.x; i < n; i += 256ll * gridDim.x) {
+    float v = to_f32(xs[i]);
+    if (trip) v = round_as<T>(fminf(fmaxf(v, -thr), thr));
+    mx = max(mx, __float_as_uint(v) & 0x7FFFFFFFu);
+  }
+  mx = wave_max_u32(mx);
+  __shared__ uint32_t red[4];
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = mx;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    mx = max(max(red[0], red[1]), max(red[2], red[3]));
+    atomicMax(reinterpret_cast<unsigned int*>(stage) + b, mx);
+  }
+}
+
+void launch_log_seqmax(const void* x, int dtype, int B, int S, int d, float* stage, int layer,
+                       const int32_t* state, int clamp_site, float clamp_thr, hipStream_t s) {
+  const dim3 grid(32, B), block(256);
+  float* st = stage + static_cast<long long>(layer) * B;
+  if (dtype == kF32)
+    hipLaunchKernelGGL(k_log_seqmax<float>, grid, block, 0, s, static_cast<const float*>(x), S, d,
+                       st, state, clamp_site, clamp_thr);
+  else if (dtype == kBF16)
+    hipLaunchKernelGGL(k_log_seqmax<bf16_t>, grid, block, 0, s, static_cast<const bf16_t*>(x), S,
+                       d, st, state, clamp_site, clamp_thr);
+  else
+    hipLaunchKernelGGL(k_log_seqmax<f16_t>, grid, block, 0, s, static_cast<const f16_t*>(x), S, d,
+                       st, state, clamp_site, clamp_thr);
 }
 
 // ------------------------------------------------------------ rotary fill
@@ -133,6 +191,38 @@ __global__ __launch_bounds__(256) void k_rope_fill(float* __restrict__ cs,
 void launch_rope_fill(float* cs, float* sn, int hd, double base,
                       const int32_t* state, hipStream_t s) {
   hipLaunchKernelGGL(k_rope_fill, dim3(256), dim3(256), 0, s, cs, sn, hd, base, state);
+}
+
+// Rows [0, rows) of one scaled frequency set (the long/short select of a
+// Phi-4-style rotary embedding): theta_i = 1 / (f_i * base^(2i/hd)) with the
+// base power rounded to fp32 and the product and quotient as fp32
+// operations; cos and sin of p * theta_i in fp64, rounded to fp32, times the
+// attention factor as an fp32 product.
+__global__ __launch_bounds__(256) void k_rope_fill_scaled(float* __restrict__ cs,
+                                                           float* __restrict__ sn, int hd,
+                                                           double base,
+                                                           const float* __restrict__ factor,
+                                                           float attn, int rows) {
+  const int half = hd / 2;
+  const long long total = static_cast<long long>(rows) * half;
+  for (long long e = blockIdx.x * 256ll + threadIdx.x; e < total;
+       e += static_cast<long long>(gridDim.x) * 256) {
+    const int p = static_cast<int>(e / half);
+    const int i = static_cast<int>(e % half);
+    const float ib = static_cast<float>(pow(base, 2.0 * static_cast<double>(i) / hd));
+    const float denom = static_cast<float>(static_cast<double>(factor[i]) * ib);
+    const double theta = static_cast<double>(static_cast<float>(1.0 / static_cast<double>(denom)));
+    const double ang = static_cast<double>(p) * theta;
+    const float c = static_cast<float>(cos(ang)), sv = static_cast<float>(sin(ang));
+    cs[e] = static_cast<float>(static_cast<double>(c) * attn);
+    sn[e] = static_cast<float>(static_cast<double>(sv) * attn);
+  }
+}
+
+void launch_rope_fill_scaled(float* cs, float* sn, int hd, double base, const float* factor,
+                             float attn, int rows, hipStream_t s) {
+  hipLaunchKernelGGL(k_rope_fill_scaled, dim3(256), dim3(256), 0, s, cs, sn, hd, base, factor,
+                     attn, rows);
 }
 
 // ------------------------------------------------------------ row kernel
@@ -290,7 +380,9 @@ void launch_rownorm(const RowArgs& a, hipStream_t s) {
 // rotary regrow, then the clamp sites in layer order), to the FIFO that the
 // host replays after the stream completes.  One thread: the order is fixed.
 __global__ void k_emit_effects(int32_t* __restrict__ state, EffectRec* __restrict__ fifo,
-                               int cap, int n_sites) {
+                               int cap, int n_sites, const float* __restrict__ log_stage,
+                               float* __restrict__ arena, int arena_cap, int n_log_layers,
+                               int B) {
   if (threadIdx.x != 0) return;
   const int fwd = state[kFwdIndex];
   const uint32_t trap = static_cast<uint32_t>(state[kTrapFwd]);
@@ -300,7 +392,9 @@ __global__ void k_emit_effects(int32_t* __restrict__ state, EffectRec* __restric
   }
   int count = state[kFifoCount];
   int dropped = state[kFifoDropped];
-  auto push = [&](int kind, int layer, int site, float value) {
+  int lcount = state[kLogCount];
+  int ldropped = state[kLogDropped];
+  auto push = [&](int kind, int layer, int site, float value, int offset, int n) {
     if (count < cap) {
       EffectRec r;
       r.forward = fwd;
@@ -308,24 +402,46 @@ __global__ void k_emit_effects(int32_t* __restrict__ state, EffectRec* __restric
       r.layer = layer;
       r.site = site;
       r.value = value;
+      r.offset = offset;
+      r.count = n;
       fifo[count] = r;
       ++count;
     } else {
       ++dropped;
     }
   };
-  if (state[kPadAny]) push(1, -1, -1, static_cast<float>(state[kPadCount]));
-  if (state[kRegrow]) push(2, -1, -1, static_cast<float>(state[kNeed]));
-  for (int i = 0; i < n_sites; ++i)
-    if (state[kClampBase + i])
-      push(3, i >> 1, i & 1, __uint_as_float(static_cast<uint32_t>(state[kAbsmaxBase + i])));
+  if (state[kPadAny]) push(1, -1, -1, static_cast<float>(state[kPadCount]), 0, 0);
+  if (state[kRegrow]) push(2, -1, -1, static_cast<float>(state[kNeed]), 0, 0);
+  const int layers = max(n_sites / 2, n_log_layers);
+  for (int l = 0; l < layers; ++l) {
+    for (int s2 = 0; s2 < 2; ++s2) {
+      const int i = 2 * l + s2;
+      if (i < n_sites && state[kClampBase + i])
+        push(3, l, s2, __uint_as_float(static_cast<uint32_t>(state[kAbsmaxBase + i])), 0, 0);
+    }
+    if (l < n_log_layers) {
+      // the tensor argument is cloned into the arena; the record points at it
+      if (lcount + B <= arena_cap) {
+        for (int b = 0; b < B; ++b) arena[lcount + b] = log_stage[l * B + b];
+        push(4, l, 0, static_cast<float>(B), lcount, B);
+        lcount += B;
+      } else {
+        ldropped += B;
+        ++dropped;
+      }
+    }
+  }
   state[kFifoCount] = count;
   state[kFifoDropped] = dropped;
+  state[kLogCount] = lcount;
+  state[kLogDropped] = ldropped;
 }
 
-void launch_emit_effects(int32_t* state, void* fifo, int cap, int n_sites, hipStream_t s) {
+void launch_emit_effects(int32_t* state, void* fifo, int cap, int n_sites, const float* log_stage,
+                         float* arena, int arena_cap, int n_log_layers, int B, hipStream_t s) {
   hipLaunchKernelGGL(k_emit_effects, dim3(1), dim3(64), 0, s, state,
-                     static_cast<EffectRec*>(fifo), cap, n_sites);
+                     static_cast<EffectRec*>(fifo), cap, n_sites, log_stage, arena, arena_cap,
+                     n_log_layers, B);
 }
 
 // ------------------------------------------------------------ row gather

@@ -63,6 +63,7 @@ struct Dec {
 };
 
 constexpr int kFifoCap = 4096;
+constexpr int kLogArenaCap = 1 << 20;   // floats of tensor log payload between flushes
 constexpr int kMaxGraphs = 8;
 
 }  // namespace
@@ -91,6 +92,7 @@ struct gm_model {
     const void *ids, *mask;
     void* logits;
     std::vector<hipGraphExec_t> execs;
+    std::vector<int> kinds;   // what the host reads after segment i (Seg::kinds)
   };
   std::vector<Frag> frags;
   bool debug_sync = false;
@@ -104,6 +106,12 @@ struct gm_model {
   float* dpart = nullptr;
   int dec_nsplit = 0;
   int cache_B = 0;          // batch of the last prefill (host-side), 0 = none
+  // `torch.equal(mask, expected)` guard (gm_set_mask_guard): device tensor and its shape
+  const int32_t* guard_expected = nullptr;
+  int guard_B = 0, guard_S = 0;
+  // tensor-valued deferred logs (cfg.log_hidden): per-forward values [L][max_batch]
+  // and the arena the effect records point into
+  float *log_stage = nullptr, *log_arena = nullptr;
 
   int alloc(void** p, size_t bytes) {
     *p = nullptr;
@@ -160,6 +168,14 @@ int validate(const gm_config* c) {
   if (c->kv_cache) {
     if (!c->causal) return inval("kv_cache needs a causal model");
     if (c->fp16_clamp) return inval("kv_cache is not supported with fp16_clamp");
+    if (c->rope_scaling) return inval("kv_cache is not supported with rope_scaling");
+  }
+  if (c->rope_scaling != GM_ROPE_PLAIN && c->rope_scaling != GM_ROPE_LONG_SHORT)
+    return inval("bad rope_scaling");
+  if (c->rope_scaling) {
+    if (c->pos != GM_POS_ROTARY) return inval("rope_scaling needs rotary positions");
+    if (c->rope_orig_max < 1) return inval("rope_orig_max must be positive");
+    if (!(c->rope_attn_factor > 0.f)) return inval("rope_attn_factor must be positive");
   }
   return GM_OK;
 }
@@ -264,7 +280,9 @@ struct Prof {
 struct Seg {
   int want = -1;
   int cur = 0;
+  std::vector<int> kinds;   // what the host reads at each cut (kCut*)
 };
+enum { kCutGuards = 0, kCutClamp = 1000, kCutLog = 2000 };
 constexpr int kCountOnly = -2;
 
 // One forward (dec == null: B x S tokens, with the KV cache filled when the
@@ -275,8 +293,11 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
              const Dec* dec = nullptr) {
   const gm_config& c = m->cfg;
   auto on = [&]() { return !seg || seg->want == -1 || seg->want == seg->cur; };
-  auto brk = [&]() {
-    if (seg) ++seg->cur;
+  auto brk = [&](int kind) {
+    if (seg) {
+      ++seg->cur;
+      seg->kinds.push_back(kind);
+    }
   };
   const int T = B * S, d = c.d_model, hd = d / c.n_heads, ff = c.d_ff;
   const int ns = n_sites(c);
@@ -295,10 +316,12 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
                            ns, m->seqlen, m->dpos, m->state, s);
   else if (on())
     launch_prologue(ids, mask, B, S, c.vocab, c.pos == GM_POS_ROTARY, c.rope_capacity, ns,
-                    m->state, s);
+                    m->guard_expected, m->guard_B == B && m->guard_S == S, m->log_stage,
+                    c.log_hidden ? c.n_layers * B : 0,
+                    c.rope_scaling ? c.rope_orig_max : 0, m->state, s);
   P(GM_K_PROLOGUE, -1, 0.0, 8.0 * T);
-  brk();  // original program: guards, mask.any() and max(position_ids) read on the host
-  if (c.pos == GM_POS_ROTARY) {
+  if (!dec) brk(kCutGuards);  // original program: guards, mask.any() and max(position_ids) read on the host
+  if (c.pos == GM_POS_ROTARY && !c.rope_scaling) {
     if (on()) launch_rope_fill(m->rope_cos, m->rope_sin, hd, c.rope_base, m->state, s);
     P(GM_K_ROPE, -1, 0.0, 0.0);
   }
@@ -351,6 +374,7 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
   ga.rope_cos = m->rope_cos;
   ga.rope_sin = m->rope_sin;
   ga.rope_rows = c.rope_capacity > 0 ? c.rope_capacity : 1;
+  ga.rope_set_stride = c.rope_scaling ? c.rope_capacity * (hd / 2) : 0;
   auto gemm = [&](int kind, const void* A, int K, const void* W, int N, int epi, const void* bias,
                   void* out, int ldo, const void* resid, int site) {
     GemmArgs q = ga;
@@ -380,7 +404,7 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
     P(kind, cur_layer, 2.0 * T * static_cast<double>(N) * K,
       es * (static_cast<double>(T) * K + static_cast<double>(N) * K +
             static_cast<double>(T) * nout * (resid ? 2 : 1)));
-    if (site >= 0) brk();  // original program: abs(h).max() read on the host
+    if (site >= 0) brk(kCutClamp + site);  // original program: abs(h).max() read on the host
   };
 
   AttnArgs at{};
@@ -483,6 +507,15 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
       gemm(GM_K_GEMM_DOWN, m->f, ff, L.w2, d, kEpiResid, L.b2, m->tmp, d, m->h, -1);
       norm_rows(m->tmp, m->h, L.ln2_g, L.ln2_b, -1);
     }
+    if (c.log_hidden) {
+      // `logger.info(..., h.abs().amax(per sequence))`: a tensor-valued log,
+      // its value taken here and replayed after the forward
+      if (on())
+        launch_log_seqmax(m->h, m->dtype, B, S, d, m->log_stage, l, m->state,
+                          pre && ns ? 2 * l + 1 : -1, thr, s);
+      P(GM_K_LOG, l, 0.0, es * T * d);
+      brk(kCutLog + l);   // original program: the value is copied to the host to print it
+    }
   }
   cur_layer = -1;
   const void* z = m->h;
@@ -496,7 +529,9 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
     P(GM_K_ARGMAX, -1, 0.0, es * B * static_cast<double>(c.vocab));
   }
   if (c.kv_cache && on()) launch_seqlen_update(m->seqlen, m->dpos, m->state, B, dec ? 1 : 0, s);
-  if (on()) launch_emit_effects(m->state, m->fifo, kFifoCap, ns, s);
+  if (on())
+    launch_emit_effects(m->state, m->fifo, kFifoCap, ns, m->log_stage, m->log_arena,
+                        kLogArenaCap, c.log_hidden ? c.n_layers : 0, B, s);
   P(GM_K_EFFECTS, -1, 0.0, 0.0);
 }
 
@@ -598,7 +633,9 @@ int gm_model_create(const gm_config* cfg, const gm_weights* w, gm_model** out) {
   if ((rc = want(w->tok_emb, true, "tok_emb")) || (rc = want(w->pos_emb, c.pos == GM_POS_LEARNED, "pos_emb")) ||
       (rc = want(w->emb_ln_g, c.emb_norm, "emb_ln_g")) || (rc = want(w->emb_ln_b, c.emb_norm && ln, "emb_ln_b")) ||
       (rc = want(w->lnf_g, pre, "lnf_g")) || (rc = want(w->lnf_b, pre && ln, "lnf_b")) ||
-      (rc = want(w->lm_head, !c.tied_head, "lm_head")))
+      (rc = want(w->lm_head, !c.tied_head, "lm_head")) ||
+      (rc = want(w->rope_short_factor, c.rope_scaling != 0, "rope_short_factor")) ||
+      (rc = want(w->rope_long_factor, c.rope_scaling != 0, "rope_long_factor")))
     return rc;
   for (int l = 0; l < c.n_layers; ++l) {
     const gm_layer_weights& L = w->layers[l];
@@ -710,10 +747,19 @@ int gm_model_create(const gm_config* cfg, const gm_weights* w, gm_model** out) {
   if ((rc = m->alloc(&p, m->n_state * sizeof(int32_t)))) return fail(rc);
   m->state = static_cast<int32_t*>(p);
   if ((rc = m->alloc(&m->fifo, kFifoCap * sizeof(EffectRec)))) return fail(rc);
+  if (c.log_hidden) {
+    if ((rc = m->alloc(&p, static_cast<size_t>(c.n_layers) * c.max_batch * sizeof(float))))
+      return fail(rc);
+    m->log_stage = static_cast<float*>(p);
+    if ((rc = m->alloc(&p, kLogArenaCap * sizeof(float)))) return fail(rc);
+    m->log_arena = static_cast<float*>(p);
+  }
   std::vector<int32_t> st(m->n_state, 0);
   st[kTrapFwd] = static_cast<int32_t>(kTrapNone);
   if (c.pos == GM_POS_ROTARY) {
-    const size_t tb = static_cast<size_t>(c.rope_capacity) * (hd / 2) * sizeof(float);
+    // long/short select: two sets, short rows first
+    const size_t sets = c.rope_scaling ? 2 : 1;
+    const size_t tb = sets * static_cast<size_t>(c.rope_capacity) * (hd / 2) * sizeof(float);
     if ((rc = m->alloc(&p, tb))) return fail(rc);
     m->rope_cos = static_cast<float*>(p);
     if ((rc = m->alloc(&p, tb))) return fail(rc);
@@ -722,12 +768,29 @@ int gm_model_create(const gm_config* cfg, const gm_weights* w, gm_model** out) {
     if (e == hipSuccess) e = hipMemset(m->rope_sin, 0, tb);
     if (e != hipSuccess) return fail(hip_fail(e, "hipMemset"));
     st[kRegrowFrom] = 0;
-    st[kRegrowTo] = c.rope_init_len;
-    st[kCachedLen] = c.rope_init_len;
+    st[kRegrowTo] = c.rope_scaling ? 0 : c.rope_init_len;
+    st[kCachedLen] = c.rope_scaling ? c.rope_capacity : c.rope_init_len;
   }
   e = hipMemcpy(m->state, st.data(), st.size() * sizeof(int32_t), hipMemcpyHostToDevice);
   if (e != hipSuccess) return fail(hip_fail(e, "state init"));
-  if (c.pos == GM_POS_ROTARY) {
+  if (c.pos == GM_POS_ROTARY && c.rope_scaling) {
+    // both frequency sets in full: the hoisted, memoised initialisation
+    const size_t half = static_cast<size_t>(c.rope_capacity) * (hd / 2);
+    float* fac = nullptr;
+    if ((rc = m->alloc(&p, 2 * (hd / 2) * sizeof(float)))) return fail(rc);
+    fac = static_cast<float*>(p);
+    e = hipMemcpy(fac, w->rope_short_factor, (hd / 2) * sizeof(float), hipMemcpyDeviceToDevice);
+    if (e == hipSuccess)
+      e = hipMemcpy(fac + hd / 2, w->rope_long_factor, (hd / 2) * sizeof(float), hipMemcpyDeviceToDevice);
+    if (e != hipSuccess) return fail(hip_fail(e, "rope factors"));
+    launch_rope_fill_scaled(m->rope_cos, m->rope_sin, hd, c.rope_base, fac, c.rope_attn_factor,
+                            c.rope_capacity, nullptr);
+    launch_rope_fill_scaled(m->rope_cos + half, m->rope_sin + half, hd, c.rope_base, fac + hd / 2,
+                            c.rope_attn_factor, c.rope_capacity, nullptr);
+    e = hipGetLastError();
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    if (e != hipSuccess) return fail(hip_fail(e, "rope init"));
+  } else if (c.pos == GM_POS_ROTARY) {
     // rows [0, rope_init_len) with the same kernel that grows the table
     launch_rope_fill(m->rope_cos, m->rope_sin, hd, c.rope_base, m->state, nullptr);
     e = hipGetLastError();
@@ -768,7 +831,7 @@ static int forward_fragmented(gm_model* m, int B, int S, const int32_t* ids,
     Seg count;
     count.want = kCountOnly;
     enqueue(m, B, S, ids, mask, logits, m->cap_stream, nullptr, &count);
-    gm_model::Frag f{B, S, ids, mask, logits, {}};
+    gm_model::Frag f{B, S, ids, mask, logits, {}, count.kinds};
     for (int i = 0; i <= count.cur; ++i) {
       hipGraph_t graph = nullptr;
       HIP_TRY(hipStreamBeginCapture(m->cap_stream, hipStreamCaptureModeThreadLocal));
@@ -805,7 +868,8 @@ static int forward_fragmented(gm_model* m, int B, int S, const int32_t* ids,
     // graph break: wait for the device, read the predicate back, branch on the host
     m->stats.host_syncs_in_forward++;
     HIP_TRY(hipStreamSynchronize(stream));
-    if (i == 0) {
+    const int kind = fr->kinds[i];
+    if (kind == kCutGuards) {
       HIP_TRY(hipMemcpy(host, m->state, sizeof(int32_t) * kClampBase, hipMemcpyDeviceToHost));
       const uint32_t trap = static_cast<uint32_t>(host[kTrapFwd]);
       if (trap != kTrapNone) {  // `if not C: raise` -- the forward stops at the guard
@@ -820,8 +884,14 @@ static int forward_fragmented(gm_model* m, int B, int S, const int32_t* ids,
       }
       m->last_host_pad_any = host[kPadAny] != 0;      // `if mask.any():`
       m->last_host_regrow = host[kRegrow] != 0;       // `if seq_len > cached:`
+    } else if (kind >= kCutLog) {
+      // `logger.info(..., tensor)`: the values come back to the host to be printed
+      float vals[1024];
+      const int n = B < 1024 ? B : 1024;
+      HIP_TRY(hipMemcpy(vals, m->log_stage + static_cast<size_t>(kind - kCutLog) * B,
+                        n * sizeof(float), hipMemcpyDeviceToHost));
     } else {
-      const int site = i - 1;
+      const int site = kind - kCutClamp;
       if (site < ns) {
         int32_t am[2];
         HIP_TRY(hipMemcpy(&am[0], m->state + kAbsmaxBase + site, sizeof(int32_t), hipMemcpyDeviceToHost));
@@ -945,6 +1015,7 @@ int gm_read_decisions(gm_model* m, gm_decisions* out, hipStream_t stream) {
     out->clamp_nan[i] = st[kNanBase + i];
   }
   out->forward_index = st[kFwdIndex];
+  out->rope_long = st[kRopeLong];
   return GM_OK;
 }
 
@@ -966,19 +1037,56 @@ int gm_check_error(gm_model* m, int32_t* code, int32_t* index) {
 int gm_flush_effects(gm_model* m, gm_effect_cb cb, void* user, int32_t* n_dropped) {
   if (!m) return inval("model is NULL");
   HIP_TRY(hipDeviceSynchronize());
-  int32_t cd[2];
+  int32_t cd[2], ld[2] = {0, 0};
   HIP_TRY(hipMemcpy(cd, m->state + kFifoCount, sizeof(cd), hipMemcpyDeviceToHost));
+  HIP_TRY(hipMemcpy(ld, m->state + kLogCount, sizeof(ld), hipMemcpyDeviceToHost));
   const int n = cd[0] < kFifoCap ? cd[0] : kFifoCap;
   std::vector<EffectRec> recs(n);
   if (n) HIP_TRY(hipMemcpy(recs.data(), m->fifo, n * sizeof(EffectRec), hipMemcpyDeviceToHost));
+  std::vector<float> arena(ld[0] > 0 ? ld[0] : 0);
+  if (!arena.empty())
+    HIP_TRY(hipMemcpy(arena.data(), m->log_arena, arena.size() * sizeof(float), hipMemcpyDeviceToHost));
   const int32_t zero[2] = {0, 0};
   HIP_TRY(hipMemcpy(m->state + kFifoCount, zero, sizeof(zero), hipMemcpyHostToDevice));
+  HIP_TRY(hipMemcpy(m->state + kLogCount, zero, sizeof(zero), hipMemcpyHostToDevice));
   if (n_dropped) *n_dropped = cd[1];
   if (cb)
     for (const EffectRec& r : recs) {
-      gm_effect e{r.forward, r.kind, r.layer, r.site, r.value};
+      gm_effect e{r.forward, r.kind, r.layer, r.site, r.value, r.count,
+                  r.count ? arena.data() + r.offset : nullptr};
       cb(&e, user);
     }
+  return GM_OK;
+}
+
+int gm_set_mask_guard(gm_model* m, const int32_t* expected, int32_t B, int32_t S) {
+  if (!m) return inval("model is NULL");
+  if (expected && (B < 1 || S < 1)) return inval("expected mask shape must be positive");
+  if (reinterpret_cast<uintptr_t>(expected) & 15) return inval("expected must be 16-byte aligned");
+  HIP_TRY(hipDeviceSynchronize());
+  // captured graphs hold the previous guard: drop them
+  for (auto& g : m->graphs) HIP_TRY(hipGraphExecDestroy(g.exec));
+  m->graphs.clear();
+  for (auto& f : m->frags)
+    for (hipGraphExec_t e : f.execs) HIP_TRY(hipGraphExecDestroy(e));
+  m->frags.clear();
+  m->guard_expected = expected;
+  m->guard_B = expected ? B : 0;
+  m->guard_S = expected ? S : 0;
+  return GM_OK;
+}
+
+int gm_trap_info(int32_t code, const char** exception_type, const char** message) {
+  static const char* const kType[] = {"", "IndexError", "ValueError", "ValueError", "IndexError",
+                                      "ValueError"};
+  static const char* const kMsg[] = {"", "token id out of range",
+                                     "attention mask values must be 0 or 1",
+                                     "rotary position exceeds the table capacity",
+                                     "sequence exceeds the KV cache capacity",
+                                     "unsupported attention mask"};
+  if (code < 1 || code > GM_TRAP_MASK_GUARD) return inval("unknown trap code");
+  if (exception_type) *exception_type = kType[code];
+  if (message) *message = kMsg[code];
   return GM_OK;
 }
 

@@ -23,8 +23,9 @@ GM_NORM_PRE, GM_NORM_POST = 0, 1
 GM_FFN_GELU, GM_FFN_GEGLU, GM_FFN_SWIGLU = 0, 1, 2
 GM_POS_NONE, GM_POS_LEARNED, GM_POS_ROTARY = 0, 1, 2
 GM_TRAP_NONE, GM_TRAP_TOKEN_RANGE, GM_TRAP_MASK_VALUE, GM_TRAP_ROPE_CAPACITY = 0, 1, 2, 3
-GM_TRAP_KV_CAPACITY = 4
-GM_EFFECT_PAD, GM_EFFECT_REGROW, GM_EFFECT_CLAMP = 1, 2, 3
+GM_TRAP_KV_CAPACITY, GM_TRAP_MASK_GUARD = 4, 5
+GM_EFFECT_PAD, GM_EFFECT_REGROW, GM_EFFECT_CLAMP, GM_EFFECT_LOG = 1, 2, 3, 4
+GM_ROPE_PLAIN, GM_ROPE_LONG_SHORT = 0, 1
 
 _i32, _f32, _u64, _vp = ctypes.c_int32, ctypes.c_float, ctypes.c_uint64, ctypes.c_void_p
 
@@ -38,7 +39,8 @@ class gm_config(ctypes.Structure):
                 ("tied_head", _i32), ("norm_eps", _f32), ("rope_base", _f32),
                 ("rope_init_len", _i32), ("rope_capacity", _i32),
                 ("act_dtype", _i32), ("fp16_clamp", _i32), ("clamp_margin", _f32),
-                ("kv_cache", _i32)]
+                ("kv_cache", _i32), ("log_hidden", _i32), ("rope_scaling", _i32),
+                ("rope_orig_max", _i32), ("rope_attn_factor", _f32)]
 
 
 LAYER_FIELDS = ["ln1_g", "ln1_b", "wqkv", "bqkv", "wo", "bo", "ln2_g", "ln2_b",
@@ -51,7 +53,8 @@ class gm_layer_weights(ctypes.Structure):
 
 
 class gm_weights(ctypes.Structure):
-    _fields_ = [(n, _vp) for n in GLOBAL_FIELDS] + [("layers", ctypes.POINTER(gm_layer_weights))]
+    _fields_ = ([(n, _vp) for n in GLOBAL_FIELDS] + [("layers", ctypes.POINTER(gm_layer_weights))]
+                + [("rope_short_factor", _vp), ("rope_long_factor", _vp)])
 
 
 class gm_decisions(ctypes.Structure):
@@ -60,12 +63,13 @@ class gm_decisions(ctypes.Structure):
                 ("clamp", _i32 * (2 * GM_MAX_LAYERS)),
                 ("clamp_absmax", _f32 * (2 * GM_MAX_LAYERS)),
                 ("clamp_nan", _i32 * (2 * GM_MAX_LAYERS)),
-                ("forward_index", _i32)]
+                ("forward_index", _i32), ("rope_long", _i32)]
 
 
 class gm_effect(ctypes.Structure):
     _fields_ = [("forward", _i32), ("kind", _i32), ("layer", _i32),
-                ("site", _i32), ("value", _f32)]
+                ("site", _i32), ("value", _f32), ("n_values", _i32),
+                ("values", ctypes.POINTER(_f32))]
 
 
 class gm_stats(ctypes.Structure):
@@ -81,12 +85,12 @@ class gm_kernel_time(ctypes.Structure):
 
 KERNEL_KINDS = ["prologue", "rope_fill", "embed", "norm", "gemm_qkv", "attention",
                 "gemm_o", "gemm_up", "gemm_down", "gemm_head", "effects", "kv_store",
-                "argmax"]
+                "argmax", "log"]
 
 gm_effect_cb = ctypes.CFUNCTYPE(None, ctypes.POINTER(gm_effect), ctypes.c_void_p)
 
 EXPORTS = ["gm_model_create", "gm_model_destroy", "gm_forward", "gm_forward_ex",
-           "gm_decode_step",
+           "gm_decode_step", "gm_set_mask_guard", "gm_trap_info",
            "gm_profile_forward", "gm_set_exec_mode", "gm_set_graph_mode", "gm_read_decisions", "gm_decisions_device_ptr",
            "gm_check_error", "gm_flush_effects", "gm_debug_buffer", "gm_get_stats",
            "gm_strerror",
@@ -111,6 +115,8 @@ def lib(path: str = LIB_PATH) -> ctypes.CDLL:
     L.gm_forward.argtypes = [_vp, _vp, _vp, _vp, _vp]
     L.gm_forward_ex.argtypes = [_vp, _i32, _i32, _vp, _vp, _vp, _vp]
     L.gm_decode_step.argtypes = [_vp, _i32, _vp, _vp, _vp, _vp]
+    L.gm_set_mask_guard.argtypes = [_vp, _vp, _i32, _i32]
+    L.gm_trap_info.argtypes = [_i32, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_char_p)]
     L.gm_set_graph_mode.argtypes = [_vp, _i32]
     L.gm_set_exec_mode.argtypes = [_vp, _i32]
     L.gm_profile_forward.argtypes = [_vp, _i32, _i32, _vp, _vp, _vp, _vp,
@@ -173,6 +179,31 @@ def gm_decode_step(m: int, B: int, ids: int, logits: int, next_ids: Optional[int
     _check(lib().gm_decode_step(m, B, ids, logits, next_ids, stream), "gm_decode_step")
 
 
+def gm_set_mask_guard(m: int, expected: Optional[int], B: int, S: int) -> None:
+    _check(lib().gm_set_mask_guard(m, expected, B, S), "gm_set_mask_guard")
+
+
+def gm_trap_info(code: int):
+    """(exception type name, message) of a trap code."""
+    t, msg = ctypes.c_char_p(), ctypes.c_char_p()
+    _check(lib().gm_trap_info(code, ctypes.byref(t), ctypes.byref(msg)), "gm_trap_info")
+    return t.value.decode(), msg.value.decode()
+
+
+_EXCEPTIONS = {"IndexError": IndexError, "ValueError": ValueError}
+
+
+def raise_trap(code: int, index: int) -> None:
+    """Re-raise a reported trap as the exception the original guard raised
+    (rule [Trap]: the uid maps back to the original type and message)."""
+    if code == GM_TRAP_NONE:
+        return
+    typ, msg = gm_trap_info(code)
+    err = _EXCEPTIONS[typ](msg)
+    err.trap_code, err.trap_index = code, index
+    raise err
+
+
 def gm_profile_forward(m: int, B: int, S: int, ids: int, mask: int, logits: int,
                        stream: int, cap: int = 4096):
     """Per-launch (kind name, layer, ms, flops, bytes) of one eager forward."""
@@ -215,7 +246,11 @@ def gm_flush_effects(m: int, cb: Optional[Callable[[gm_effect], None]] = None):
 
     def _cb(p, _user):
         e = p.contents
-        recs.append((e.forward, e.kind, e.layer, e.site, e.value))
+        if e.n_values:
+            recs.append((e.forward, e.kind, e.layer, e.site, e.value,
+                         tuple(e.values[i] for i in range(e.n_values))))
+        else:
+            recs.append((e.forward, e.kind, e.layer, e.site, e.value))
         if cb is not None:
             cb(e)
 

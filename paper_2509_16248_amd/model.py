@@ -34,7 +34,12 @@ def make_config(c, max_batch: Optional[int] = None, max_seq: Optional[int] = Non
         tied_head=int(c.tied_head), norm_eps=c.norm_eps, rope_base=c.rope_base,
         rope_init_len=c.rope_init_len, rope_capacity=c.rope_capacity,
         act_dtype=_DTYPES[c.dtype], fp16_clamp=int(c.fp16_clamp),
-        clamp_margin=c.clamp_margin, kv_cache=int(kv_cache))
+        clamp_margin=c.clamp_margin, kv_cache=int(kv_cache),
+        log_hidden=int(getattr(c, "log_hidden", False)),
+        rope_scaling={"none": gm.GM_ROPE_PLAIN, "long_short": gm.GM_ROPE_LONG_SHORT}[
+            getattr(c, "rope_scaling", "none")],
+        rope_orig_max=int(getattr(c, "rope_orig_max", 0)),
+        rope_attn_factor=float(getattr(c, "rope_attn_factor", 1.0)))
 
 
 def to_device(a: np.ndarray, dtype: str, device) -> torch.Tensor:
@@ -80,6 +85,12 @@ class GmModel:
                 keep.append(t)
                 setattr(arr[l], name, t.data_ptr() if t is not None else None)
         w.layers = ctypes.cast(arr, ctypes.POINTER(gm.gm_layer_weights))
+        for name in ("rope_short_factor", "rope_long_factor"):
+            x = globals_.get(name)
+            if x is not None:
+                t = torch.as_tensor(np.asarray(x, dtype=np.float32)).to(self.device)
+                keep.append(t)
+                setattr(w, name, t.data_ptr())
         torch.cuda.synchronize(self.device)
         with torch.cuda.device(self.device):
             self.handle = gm.gm_model_create(self.c, w)
@@ -144,10 +155,28 @@ class GmModel:
                 "cached_len": d.cached_len, "forward_index": d.forward_index,
                 "clamp": [bool(d.clamp[i]) for i in range(n)],
                 "clamp_absmax": [d.clamp_absmax[i] for i in range(n)],
-                "clamp_nan": [bool(d.clamp_nan[i]) for i in range(n)]}
+                "clamp_nan": [bool(d.clamp_nan[i]) for i in range(n)],
+                "rope_long": bool(d.rope_long)}
 
     def check_error(self):
         return gm.gm_check_error(self.handle)
+
+    def raise_on_trap(self):
+        """Synchronise, and if a guard failed since the last check raise the
+        exception the original guard raises (gm_trap_info)."""
+        code, index = gm.gm_check_error(self.handle)
+        gm.raise_trap(code, index)
+
+    def set_mask_guard(self, expected: Optional[torch.Tensor]):
+        """`if not torch.equal(attention_mask, expected): raise` on every
+        later forward (None removes it).  Keeps a reference to ``expected``."""
+        if expected is None:
+            gm.gm_set_mask_guard(self.handle, None, 0, 0)
+            self._guard = None
+            return
+        assert expected.dtype == torch.int32 and expected.dim() == 2 and expected.is_contiguous()
+        self._guard = expected
+        gm.gm_set_mask_guard(self.handle, expected.data_ptr(), *expected.shape)
 
     def flush_effects(self):
         return gm.gm_flush_effects(self.handle)

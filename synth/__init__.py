@@ -24,6 +24,9 @@ for them:
 * ``decoder_4096``      32 layers, d=4096, 32 heads, SwiGLU FFN 11008,
                         RMSNorm, rotary (base 1e4, cache 1024 grown on
                         demand), vocab 32000, batch 1 x seq 2048, bf16
+* ``decoder_4096_longrope`` the same shape with a Phi-4-style long/short
+                        rotary frequency select (original context 1024:
+                        2048 positions take the long factors)
 
 Weights: every tensor is drawn from its own PCG64 stream seeded by
 ``SeedSequence([seed, tensor_index])``; matrices, embeddings and biases are
@@ -77,6 +80,10 @@ class ModelConfig:
     outlier_frac: float = 0.0
     outlier_scale: float = 1.0
     max_pad: int = 0
+    log_hidden: bool = False          # per-layer tensor-valued log (max |h| per sequence)
+    rope_scaling: str = "none"        # "none" or "long_short"
+    rope_orig_max: int = 0            # long factors when max(position) + 1 exceeds this
+    rope_attn_factor: float = 1.0     # cos/sin scale of the scaled frequencies
 
     @property
     def head_dim(self) -> int:
@@ -126,6 +133,20 @@ PRESETS: Dict[str, ModelConfig] = {
 }
 
 
+def _longrope(base: ModelConfig, orig: int) -> ModelConfig:
+    """``base`` with the long/short frequency select; the tables hold the
+    whole capacity, and cos/sin are scaled by sqrt(1 + ln(c/o)/ln(o))."""
+    import math
+    cap = base.rope_capacity
+    attn = math.sqrt(1.0 + math.log(cap / orig) / math.log(orig)) if cap > orig else 1.0
+    return base.replace(rope_scaling="long_short", rope_orig_max=orig,
+                        rope_attn_factor=float(np.float32(attn)), rope_init_len=cap)
+
+
+PRESETS["decoder_4096_longrope"] = _longrope(PRESETS["decoder_4096"], 1024).replace(
+    name="decoder_4096_longrope")
+
+
 def preset(name: str, **overrides) -> ModelConfig:
     return PRESETS[name].replace(**overrides)
 
@@ -166,7 +187,9 @@ def encode(x: np.ndarray, dtype: str) -> np.ndarray:
 # Fixed tensor indices so that every tensor has its own random stream and a
 # layer's weights can be regenerated without drawing the others.
 GLOBAL_TENSORS = ["tok_emb", "pos_emb", "emb_ln_g", "emb_ln_b", "lnf_g",
-                  "lnf_b", "lm_head"]
+                  "lnf_b", "lm_head", "rope_short_factor", "rope_long_factor"]
+# rotary frequency factors: float32 whatever the storage dtype
+ROPE_FACTORS = {"rope_short_factor", "rope_long_factor"}
 LAYER_TENSORS = ["ln1_g", "ln1_b", "wqkv", "bqkv", "wo", "bo", "ln2_g",
                  "ln2_b", "w1", "b1", "w2", "b2"]
 MATRICES = {"tok_emb", "pos_emb", "lm_head", "wqkv", "wo", "w1", "w2"}
@@ -194,6 +217,9 @@ def tensor_shapes(cfg: ModelConfig) -> Dict[str, tuple]:
             s["lnf_b"] = (d,)
     if not cfg.tied_head:
         s["lm_head"] = (V, d)
+    if cfg.rope_scaling == "long_short":
+        s["rope_short_factor"] = (cfg.head_dim // 2,)
+        s["rope_long_factor"] = (cfg.head_dim // 2,)
     return s
 
 
@@ -216,6 +242,13 @@ def _draw(cfg: ModelConfig, seed: int, name: str, layer: Optional[int],
           shape: tuple) -> np.ndarray:
     rng = np.random.Generator(np.random.PCG64(
         np.random.SeedSequence([seed, _tensor_index(name, layer)])))
+    if name in ROPE_FACTORS:
+        # per-frequency factors shaped like a long-context rope: short ones
+        # near 1, long ones growing from ~1 (fast frequencies) to ~16 (slow)
+        u = np.sort(rng.random(shape, dtype=np.float32))
+        if name == "rope_short_factor":
+            return np.float32(1.0) + np.float32(0.25) * u
+        return np.float32(1.0) + np.float32(15.0) * u * u
     x = rng.standard_normal(shape, dtype=np.float32) * np.float32(cfg.sigma)
     if name.endswith("_g"):
         x += np.float32(1.0)
@@ -310,4 +343,7 @@ def reduced(name: str) -> ModelConfig:
         return base.replace(n_layers=2, d_model=512, n_heads=4, d_ff=1344,
                             batch=1, seq=300, vocab=1100, rope_init_len=128,
                             rope_capacity=512)
+    if name == "decoder_4096_longrope":
+        small = reduced("decoder_4096").replace(name=name)
+        return _longrope(small, 128)
     raise KeyError(name)

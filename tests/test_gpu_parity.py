@@ -51,10 +51,15 @@ def effects_of(res):
     return [(e.forward, e.kind, e.layer, e.site, np.float32(e.value)) for e in res.effects]
 
 
-def gpu_effects(model):
+def gpu_effects(model, with_values=False):
+    """Deferred effects as (forward, kind, layer, site, value) tuples; with
+    ``with_values`` a sixth entry holds a log record's tensor values."""
     recs, dropped = model.flush_effects()
     assert dropped == 0
-    return [(f, k, l, s, np.float32(v)) for f, k, l, s, v in recs]
+    if with_values:
+        return [(r[0], r[1], r[2], r[3], np.float32(r[4]), r[5] if len(r) > 5 else None)
+                for r in recs]
+    return [(r[0], r[1], r[2], r[3], np.float32(r[4])) for r in recs]
 
 
 def check_decisions(dec, res, cfg):
