@@ -196,7 +196,7 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=2)
+    ap.add_argument("--cpu-rows", type=int, default=8)
     ap.add_argument("--no-fragmented", action="store_true",
                     help="skip the graph-broken baseline (same kernels, host sync per break)")
     ap.add_argument("--no-decode", action="store_true", help="skip the KV-cache decode measurement")
