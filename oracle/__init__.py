@@ -17,10 +17,11 @@ from .model import (EFFECT_CLAMP, EFFECT_LOG, EFFECT_PAD, EFFECT_REGROW, FP16_MA
                     TRAP_TOKEN_RANGE, Effect, OracleModel, OracleResult, Trap)
 from .decode import DecodeStep, OracleDecoder, generate_greedy, greedy
 from .model import TRAP_KV_CAPACITY
+from .seq2seq import OracleSeq2Seq, Seq2SeqResult
 from . import numerics
 
 __all__ = ["OracleModel", "OracleResult", "Trap", "Effect", "numerics",
            "TRAP_TOKEN_RANGE", "TRAP_MASK_VALUE", "TRAP_ROPE_CAPACITY",
            "EFFECT_PAD", "EFFECT_REGROW", "EFFECT_CLAMP", "FP16_MAX",
            "OracleDecoder", "DecodeStep", "generate_greedy", "greedy", "TRAP_KV_CAPACITY",
-           "TRAP_MASK_GUARD", "TRAP_INFO", "EFFECT_LOG"]
+           "TRAP_MASK_GUARD", "TRAP_INFO", "EFFECT_LOG", "OracleSeq2Seq", "Seq2SeqResult"]

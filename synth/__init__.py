@@ -27,6 +27,11 @@ for them:
 * ``decoder_4096_longrope`` the same shape with a Phi-4-style long/short
                         rotary frequency select (original context 1024:
                         2048 positions take the long factors)
+* ``seq2seq_768``       encoder-decoder (BART-base-shaped, pre-LN): 6 encoder
+                        + 6 decoder layers with cross-attention, d=768, 12
+                        heads, FFN 3072 GELU, learned positions, shared
+                        embedding and head, vocab 50265, batch 8, source 512
+                        (0..128 pads), target 128 (0..32 pads), bf16
 
 Weights: every tensor is drawn from its own PCG64 stream seeded by
 ``SeedSequence([seed, tensor_index])``; matrices, embeddings and biases are
@@ -84,6 +89,9 @@ class ModelConfig:
     rope_scaling: str = "none"        # "none" or "long_short"
     rope_orig_max: int = 0            # long factors when max(position) + 1 exceeds this
     rope_attn_factor: float = 1.0     # cos/sin scale of the scaled frequencies
+    n_dec_layers: int = 0             # > 0: encoder-decoder (n_layers encoder layers)
+    tgt_seq: int = 0                  # encoder-decoder: target positions
+    tgt_max_pad: int = 0              # encoder-decoder: trailing pads of a target
 
     @property
     def head_dim(self) -> int:
@@ -131,6 +139,31 @@ PRESETS: Dict[str, ModelConfig] = {
         norm_eps=1e-6, rope_base=10000.0, rope_init_len=1024,
         rope_capacity=4096, max_pad=0),
 }
+
+
+PRESETS["seq2seq_768"] = ModelConfig(
+    name="seq2seq_768", n_layers=6, n_dec_layers=6, d_model=768, n_heads=12, d_ff=3072,
+    vocab=50265, batch=8, seq=512, tgt_seq=128, dtype=BF16, norm=LN, norm_place=PRE,
+    ffn=GELU, pos=POS_LEARNED, causal=True, bias=True, tied_head=True, max_pad=128,
+    tgt_max_pad=32)
+
+
+def make_target_inputs(cfg: ModelConfig, seed: int, batch: Optional[int] = None,
+                       seq: Optional[int] = None, max_pad: Optional[int] = None):
+    """Decoder inputs of an encoder-decoder workload: ids and a trailing-pad
+    mask [B, tgt_seq], from a stream of their own."""
+    B = cfg.batch if batch is None else batch
+    S = cfg.tgt_seq if seq is None else seq
+    P = cfg.tgt_max_pad if max_pad is None else max_pad
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 7, 1])))
+    ids = rng.integers(0, cfg.vocab, size=(B, S), dtype=np.int64).astype(np.int32)
+    mask = np.ones((B, S), dtype=np.int32)
+    if P > 0:
+        pads = rng.integers(0, min(P, S - 1) + 1, size=B)
+        for b in range(B):
+            if pads[b]:
+                mask[b, S - pads[b]:] = 0
+    return ids, mask
 
 
 def _longrope(base: ModelConfig, orig: int) -> ModelConfig:
@@ -187,17 +220,23 @@ def encode(x: np.ndarray, dtype: str) -> np.ndarray:
 # Fixed tensor indices so that every tensor has its own random stream and a
 # layer's weights can be regenerated without drawing the others.
 GLOBAL_TENSORS = ["tok_emb", "pos_emb", "emb_ln_g", "emb_ln_b", "lnf_g",
-                  "lnf_b", "lm_head", "rope_short_factor", "rope_long_factor"]
+                  "lnf_b", "lm_head", "rope_short_factor", "rope_long_factor",
+                  "enc_pos_emb", "enc_lnf_g", "enc_lnf_b"]
+# an encoder-decoder's decoder layer: the layer tensors plus its cross-attention
+CROSS_TENSORS = ["x_lnc_g", "x_lnc_b", "x_wq", "x_bq", "x_wkv", "x_bkv", "x_wo", "x_bo"]
 # rotary frequency factors: float32 whatever the storage dtype
 ROPE_FACTORS = {"rope_short_factor", "rope_long_factor"}
 LAYER_TENSORS = ["ln1_g", "ln1_b", "wqkv", "bqkv", "wo", "bo", "ln2_g",
                  "ln2_b", "w1", "b1", "w2", "b2"]
-MATRICES = {"tok_emb", "pos_emb", "lm_head", "wqkv", "wo", "w1", "w2"}
+MATRICES = {"tok_emb", "pos_emb", "lm_head", "wqkv", "wo", "w1", "w2", "enc_pos_emb", "x_wq",
+            "x_wkv", "x_wo"}
 
 
-def _tensor_index(name: str, layer: Optional[int]) -> int:
+def _tensor_index(name: str, layer) -> int:
     if layer is None:
         return GLOBAL_TENSORS.index(name)
+    if isinstance(layer, tuple):        # ("dec", l): decoder layer of an encoder-decoder
+        return 2000 + 32 * layer[1] + (LAYER_TENSORS + CROSS_TENSORS).index(name)
     return 100 + 16 * layer + LAYER_TENSORS.index(name)
 
 
@@ -206,7 +245,12 @@ def tensor_shapes(cfg: ModelConfig) -> Dict[str, tuple]:
     d, V = cfg.d_model, cfg.vocab
     s = {"tok_emb": (V, d)}
     if cfg.pos == POS_LEARNED:
-        s["pos_emb"] = (cfg.seq, d)
+        s["pos_emb"] = (cfg.tgt_seq if cfg.n_dec_layers else cfg.seq, d)
+    if cfg.n_dec_layers:
+        s["enc_pos_emb"] = (cfg.seq, d)
+        s["enc_lnf_g"] = (d,)
+        if cfg.norm == LN:
+            s["enc_lnf_b"] = (d,)
     if cfg.emb_norm:
         s["emb_ln_g"] = (d,)
         if cfg.norm == LN:
@@ -235,6 +279,18 @@ def layer_shapes(cfg: ModelConfig) -> Dict[str, tuple]:
         s["ln2_b"] = (d,)
     if cfg.bias:
         s.update({"bqkv": (3 * d,), "bo": (d,), "b1": (f1,), "b2": (d,)})
+    return s
+
+
+def cross_shapes(cfg: ModelConfig) -> Dict[str, tuple]:
+    """Cross-attention tensors of an encoder-decoder's decoder layer
+    (``x_wkv`` holds the k rows, then the v rows)."""
+    d = cfg.d_model
+    s = {"x_lnc_g": (d,), "x_wq": (d, d), "x_wkv": (2 * d, d), "x_wo": (d, d)}
+    if cfg.norm == LN:
+        s["x_lnc_b"] = (d,)
+    if cfg.bias:
+        s.update({"x_bq": (d,), "x_bkv": (2 * d,), "x_bo": (d,)})
     return s
 
 
@@ -281,9 +337,11 @@ class Weights:
     seed: int
     globals: Dict[str, np.ndarray]
     layers: List[Dict[str, np.ndarray]]
+    dec_layers: List[Dict[str, np.ndarray]] = dataclasses.field(default_factory=list)
 
     def nbytes(self) -> int:
         n = sum(v.nbytes for v in self.globals.values())
+        n += sum(v.nbytes for L in self.dec_layers for v in L.values())
         return n + sum(v.nbytes for L in self.layers for v in L.values())
 
 
@@ -295,13 +353,22 @@ def make_weights(cfg: ModelConfig, seed: int = 1234, threads: Optional[int] = No
     tasks = [(k, None, shp) for k, shp in tensor_shapes(cfg).items()]
     for l in range(cfg.n_layers):
         tasks += [(k, l, shp) for k, shp in layer_shapes(cfg).items()]
+    for l in range(cfg.n_dec_layers):
+        shapes = dict(layer_shapes(cfg), **cross_shapes(cfg))
+        tasks += [(k, ("dec", l), shp) for k, shp in shapes.items()]
     n = threads or min(16, len(os.sched_getaffinity(0)))
     with cf.ThreadPoolExecutor(max_workers=max(1, n)) as ex:
         arrays = list(ex.map(lambda t: _draw(cfg, seed, t[0], t[1], t[2]), tasks))
     glob, layers = {}, [dict() for _ in range(cfg.n_layers)]
+    dec = [dict() for _ in range(cfg.n_dec_layers)]
     for (k, l, _), a in zip(tasks, arrays):
-        (glob if l is None else layers[l])[k] = a
-    return Weights(cfg, seed, glob, layers)
+        if l is None:
+            glob[k] = a
+        elif isinstance(l, tuple):
+            dec[l[1]][k] = a
+        else:
+            layers[l][k] = a
+    return Weights(cfg, seed, glob, layers, dec)
 
 
 # ---------------------------------------------------------------- inputs
@@ -343,6 +410,9 @@ def reduced(name: str) -> ModelConfig:
         return base.replace(n_layers=2, d_model=512, n_heads=4, d_ff=1344,
                             batch=1, seq=300, vocab=1100, rope_init_len=128,
                             rope_capacity=512)
+    if name == "seq2seq_768":
+        return base.replace(n_layers=2, n_dec_layers=2, batch=3, seq=96, tgt_seq=40,
+                            vocab=1000, max_pad=30, tgt_max_pad=10)
     if name == "decoder_4096_longrope":
         small = reduced("decoder_4096").replace(name=name)
         return _longrope(small, 128)
