@@ -100,6 +100,68 @@ def break_suite(args):
         torch.cuda.empty_cache()
 
 
+def seq2seq_bench(args):
+    """The encoder-decoder workload (6 + 6 layers, d 768, batch 8, source 512,
+    target 128, ragged): single-graph forwards timed with events, then the
+    graph-broken program on the same buffers.  Throughput counts source and
+    target positions."""
+    import torch
+    import synth
+    from paper_2509_16248_amd.model import GmModel
+    cfg = synth.preset("seq2seq_768")
+    w = synth.make_weights(cfg, 1234)
+    si, sm = synth.make_inputs(cfg, 0)
+    ti, tm = synth.make_target_inputs(cfg, 0)
+    m = GmModel(cfg, w.globals, w.layers, dec_layers=w.dec_layers, device="cuda:0")
+    del w
+    bufs = [torch.from_numpy(a).cuda() for a in (si, sm, ti, tm)]
+    out = m.new_logits(cfg.batch, cfg.tgt_seq)
+    stream = torch.cuda.current_stream()
+
+    def loop(n):
+        for _ in range(n):
+            m.forward_seq2seq(*bufs, out)
+
+    def timed(mode):
+        m.set_exec_mode(mode)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        loop(1)
+        torch.cuda.synchronize()
+        cold = (time.perf_counter() - t0) * 1e3
+        loop(args.warmup)
+        torch.cuda.synchronize()
+        s0 = m.stats()
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        ev0.record(stream)
+        loop(args.steps)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        wall = (time.perf_counter() - t0) * 1e3 / args.steps
+        s1 = m.stats()
+        return {"ms_per_step": round(ev0.elapsed_time(ev1) / args.steps, 4),
+                "wall_ms_per_step": round(wall, 4), "cold_ms": round(cold, 2),
+                "graph_launches_per_forward": (s1["graph_launches"] - s0["graph_launches"]) / args.steps,
+                "host_syncs_per_forward": (s1["host_syncs_in_forward"] - s0["host_syncs_in_forward"]) / args.steps}
+
+    g = timed("graph")
+    f = timed("fragmented")
+    code = m.check_error()
+    kernels = m.stats()["kernels_per_forward"]
+    m.close()
+    tokens = cfg.batch * (cfg.seq + cfg.tgt_seq)
+    return {"workload": "seq2seq_768: 6 encoder + 6 decoder layers (cross-attention), d_model 768, "
+                        "12 heads, FFN 3072 GELU, pre-LN, vocab 50265, bf16; batch 8, source 512 "
+                        "(0..128 pads), target 128 (0..32 pads)",
+            "tokens_per_forward": tokens, "kernels_per_forward": kernels,
+            "tokens_per_s": round(tokens / (g["ms_per_step"] * 1e-3), 1),
+            "single_graph": g, "fragmented": f,
+            "steady_speedup": round(f["wall_ms_per_step"] / g["wall_ms_per_step"], 3),
+            "trap": list(code)}
+
+
 def decode_bench(cfg, w, prompt=384, steps=120, warmup=8):
     """Greedy decoding with the KV cache on the benchmarked model: prefill
     B x ``prompt`` positions (ragged, 0..128 trailing pads), then ``steps``
@@ -200,6 +262,8 @@ def main():
     ap.add_argument("--no-fragmented", action="store_true",
                     help="skip the graph-broken baseline (same kernels, host sync per break)")
     ap.add_argument("--no-decode", action="store_true", help="skip the KV-cache decode measurement")
+    ap.add_argument("--no-seq2seq", action="store_true",
+                    help="skip the encoder-decoder measurement")
     ap.add_argument("--break-suite", action="store_true",
                     help="only compare single-graph and graph-broken forwards on every workload")
     args = ap.parse_args()
@@ -316,6 +380,10 @@ def main():
         torch.cuda.empty_cache()
         result["decode"] = decode_bench(cfg, w)
         log(f"[bench] decode: {result['decode']}")
+    if not args.no_seq2seq:
+        torch.cuda.empty_cache()
+        result["seq2seq"] = seq2seq_bench(args)
+        log(f"[bench] seq2seq: {result['seq2seq']}")
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a sample")
         result["cpu_baseline"] = cpu_baseline(cfg, w, ids, mask, list(range(args.cpu_rows)))

@@ -95,6 +95,14 @@ enum { GM_ROPE_PLAIN = 0, GM_ROPE_LONG_SHORT = 1 };
  *  (rule [Where]: both tables are built at create, a device flag selects);
  *  cos and sin are scaled by rope_attn_factor.  The regrow predicate does
  *  not apply: both tables hold rope_capacity rows from the start.
+ *  n_dec_layers > 0 makes an encoder-decoder model (gm_forward_seq2seq):
+ *  n_layers bidirectional pre-norm encoder layers over max_seq source
+ *  positions (learned positions enc_pos_emb, final norm enc_lnf), then
+ *  n_dec_layers pre-norm decoder layers over max_tgt target positions, each
+ *  with causal self-attention, cross-attention to the encoder output and the
+ *  FFN; the token embedding is shared by both stacks.  Needs norm_place PRE,
+ *  pos LEARNED, causal, and none of fp16_clamp, kv_cache, log_hidden,
+ *  rope_scaling, emb_norm.
  */
 typedef struct gm_config {
   int32_t abi_version;      /* must be GM_ABI_VERSION */
@@ -112,6 +120,7 @@ typedef struct gm_config {
   int32_t rope_scaling;
   int32_t rope_orig_max;
   float   rope_attn_factor;
+  int32_t n_dec_layers, max_tgt;
 } gm_config;
 
 /* ------------------------------------------------------------ weights
@@ -132,10 +141,26 @@ typedef struct gm_layer_weights {
   const void *ln2_g, *ln2_b, *w1, *b1, *w2, *b2;
 } gm_layer_weights;
 
+/* Cross-attention of one decoder layer (encoder-decoder models):
+ *  lnc_g / lnc_b [d]      pre-norm of the cross-attention block
+ *  wq [d, d], bq [d]      query projection of the decoder stream
+ *  wkv [2d, d], bkv [2d]  key and value projection of the encoder output
+ *                         (rows: k (d), then v (d))
+ *  wo [d, d], bo [d]      output projection (added to the decoder residual) */
+typedef struct gm_cross_weights {
+  const void *lnc_g, *lnc_b, *wq, *bq, *wkv, *bkv, *wo, *bo;
+} gm_cross_weights;
+
 typedef struct gm_weights {
   const void *tok_emb, *pos_emb, *emb_ln_g, *emb_ln_b, *lnf_g, *lnf_b, *lm_head;
   const gm_layer_weights *layers;   /* host array of n_layers entries */
   const float *rope_short_factor, *rope_long_factor;   /* device fp32 [hd/2], rope_scaling only */
+  /* encoder-decoder models: layers are the encoder's n_layers layers;
+   * pos_emb [max_tgt, d] and lnf_* are the decoder's; tok_emb (and lm_head)
+   * are shared */
+  const void *enc_pos_emb, *enc_lnf_g, *enc_lnf_b;  /* [max_seq, d], [d], [d] */
+  const gm_layer_weights *dec_layers;               /* host array, n_dec_layers */
+  const gm_cross_weights *dec_cross;                /* host array, n_dec_layers */
 } gm_weights;
 
 typedef struct gm_model gm_model;
@@ -152,6 +177,8 @@ typedef struct gm_decisions {
   int32_t clamp_nan[2 * GM_MAX_LAYERS];    /* some element of h was NaN     */
   int32_t forward_index;  /* 0-based count of forwards enqueued before it     */
   int32_t rope_long;      /* rope_scaling: the long frequency set was used    */
+  int32_t pad_any_tgt;    /* encoder-decoder: the target mask had a 0 (pad_any
+                             is then the source's)                          */
 } gm_decisions;
 
 /* One deferred effect: what the original program would have printed. */
@@ -172,7 +199,8 @@ typedef void (*gm_effect_cb)(const gm_effect *effect, void *user);
 enum { GM_K_PROLOGUE = 0, GM_K_ROPE = 1, GM_K_EMBED = 2, GM_K_NORM = 3,
        GM_K_GEMM_QKV = 4, GM_K_ATTENTION = 5, GM_K_GEMM_O = 6, GM_K_GEMM_UP = 7,
        GM_K_GEMM_DOWN = 8, GM_K_GEMM_HEAD = 9, GM_K_EFFECTS = 10, GM_K_KV_STORE = 11,
-       GM_K_ARGMAX = 12, GM_K_LOG = 13 };
+       GM_K_ARGMAX = 12, GM_K_LOG = 13, GM_K_GEMM_XQ = 14, GM_K_GEMM_XKV = 15,
+       GM_K_GEMM_XO = 16, GM_K_XATTN = 17 };
 
 /* One kernel launch of a profiled forward.  flops/bytes are the launch's
  * algorithmic work (2*M*N*K for a GEMM; 4*hd*visible (query,key) pairs per
@@ -253,6 +281,21 @@ int gm_forward_ex(gm_model *m, int32_t B, int32_t S, const int32_t *token_ids,
  * and is recorded as a deferred effect.  Not available in fragmented mode. */
 int gm_decode_step(gm_model *m, int32_t B, const int32_t *token_ids, void *out_logits,
                    int32_t *next_ids, hipStream_t stream);
+
+/* Encoder-decoder forward (n_dec_layers > 0): the encoder over
+ * src_ids/src_mask [B, S_src] (S_src <= max_seq), then the decoder over
+ * tgt_ids/tgt_mask [B, S_tgt] (S_tgt <= max_tgt) attending to the encoder
+ * output; out_logits [B, S_tgt, vocab].  Device int32 inputs, 16-byte
+ * aligned pointers, one graph launch per call as gm_forward.  Each mask has
+ * its own `mask.any()` branch (source: encoder self-attention and the
+ * decoder's cross-attention; target: decoder self-attention), recorded as PAD
+ * effects with site 0 (source) and 1 (target).  Guards: token ids, then
+ * mask values, each over the source followed by the target (the position
+ * of a target element is B * S_src + its row-major index).  Graph and eager
+ * execution; not in fragmented mode. */
+int gm_forward_seq2seq(gm_model *m, int32_t B, int32_t S_src, const int32_t *src_ids,
+                       const int32_t *src_mask, int32_t S_tgt, const int32_t *tgt_ids,
+                       const int32_t *tgt_mask, void *out_logits, hipStream_t stream);
 
 /* Run one forward without a graph, recording a HIP event on `stream` after
  * every kernel, wait for it, and write one gm_kernel_time per launch (in

@@ -7,10 +7,12 @@
 // flag set, key tiles at or past 1 + the last unmasked key of the sequence
 // are skipped.  Causal models see keys j <= i.
 //
-// q, k and v are read in place from the fused projection output
-// [B*S, 3d] (q | k | v, head h at columns h*hd); the context is written as
-// [B*S, d] with head h at columns h*hd, the layout the output projection
-// reads.
+// q, k and v are read in place from row-major activations with given row
+// strides: for self-attention all three from the fused projection output
+// [B*S, 3d] (q | k | v, head h at columns h*hd); for cross-attention q from
+// the decoder's [B*Sq, d] projection and k | v from [B*Sk, 2d] projected from
+// the encoder output.  The context is written as [B*Sq, d] with head h at
+// columns h*hd, the layout the output projection reads.
 #include <math.h>
 
 #include "gm_device.h"
@@ -31,23 +33,24 @@ __global__ __launch_bounds__(64) void k_attn_rows(AttnArgs a) {
   extern __shared__ float sm[];
   const int i = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int lane = threadIdx.x;
-  const int S = a.S, hd = a.hd, ld = 3 * a.d;
+  const int Sk = a.Sk, hd = a.hd;
   float* sq = sm;           // [hd]
-  float* sp = sm + hd;      // [S]
-  const T* base = static_cast<const T*>(a.qkv) + static_cast<long long>(b) * S * ld;
-  const T* q = base + static_cast<long long>(i) * ld + h * hd;
+  float* sp = sm + hd;      // [Sk]
+  const T* q = static_cast<const T*>(a.q) + (static_cast<long long>(b) * a.Sq + i) * a.ldq + h * hd;
+  const T* kb = static_cast<const T*>(a.k) + static_cast<long long>(b) * Sk * a.ldkv + h * hd;
+  const T* vb = static_cast<const T*>(a.v) + static_cast<long long>(b) * Sk * a.ldkv + h * hd;
   for (int c = lane; c < hd; c += 64) sq[c] = to_f32(q[c]);
-  const int pad = a.state[kPadAny];
-  int kend = pad ? a.state[kKvLenBase + b] : S;
+  const int pad = a.state[a.pad_slot];
+  int kend = pad ? a.state[a.kvlen_base + b] : Sk;
   if (a.causal) kend = kend < i + 1 ? kend : i + 1;
-  const int32_t* mk = a.mask + static_cast<long long>(b) * S;
+  const int32_t* mk = a.mask + static_cast<long long>(b) * Sk;
   __syncthreads();
   float lmax = -INFINITY;
   for (int j = lane; j < kend; j += 64) {
     const bool ok = !pad || mk[j] != 0;
     float s = -INFINITY;
     if (ok) {
-      const T* k = base + static_cast<long long>(j) * ld + a.d + h * hd;
+      const T* k = kb + static_cast<long long>(j) * a.ldkv;
       float acc = 0.f;
       for (int c = 0; c < hd; ++c) acc = fmaf(sq[c], to_f32(k[c]), acc);
       s = acc * a.scale;
@@ -65,12 +68,12 @@ __global__ __launch_bounds__(64) void k_attn_rows(AttnArgs a) {
   }
   const float l = wave_sum(lsum);
   __syncthreads();
-  T* out = static_cast<T*>(a.ctx) + (static_cast<long long>(b) * S + i) * a.d + h * hd;
+  T* out = static_cast<T*>(a.ctx) + (static_cast<long long>(b) * a.Sq + i) * a.d + h * hd;
   for (int c = lane; c < hd; c += 64) {
     float o = 0.f;
     for (int j = 0; j < kend; ++j) {
       const float p = sp[j];
-      if (p != 0.f) o = fmaf(p, to_f32(base[static_cast<long long>(j) * ld + 2 * a.d + h * hd + c]), o);
+      if (p != 0.f) o = fmaf(p, to_f32(vb[static_cast<long long>(j) * a.ldkv + c]), o);
     }
     out[c] = from_f32<T>(l > 0.f ? o / l : 0.f);
   }
@@ -122,15 +125,14 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) T sK[2][kKB * LDK];
   __shared__ __attribute__((aligned(16))) T sVt[2][HD * LDV];
   __shared__ int sMask[2][kKB];
-  const int nqb = (a.S + kQB - 1) / kQB;
+  const int nqb = (a.Sq + kQB - 1) / kQB;
   const int qb = a.causal ? nqb - 1 - static_cast<int>(blockIdx.x) : static_cast<int>(blockIdx.x);
   const int h = blockIdx.y, b = blockIdx.z;
-  const int S = a.S, d = a.d, ld = 3 * d;
+  const int Sq = a.Sq, S = a.Sk, d = a.d, ld = a.ldkv;
   const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
   const int l16 = lane & 15, g = lane >> 4;
-  const T* base = static_cast<const T*>(a.qkv) + static_cast<long long>(b) * S * ld;
-  const T* kbase = base + d + h * HD;
-  const T* vbase = base + 2 * d + h * HD;
+  const T* kbase = static_cast<const T*>(a.k) + static_cast<long long>(b) * S * ld + h * HD;
+  const T* vbase = static_cast<const T*>(a.v) + static_cast<long long>(b) * S * ld + h * HD;
   const int32_t* mk = a.mask + static_cast<long long>(b) * S;
   const int q0 = qb * kQB + wave * 32;
 
@@ -138,16 +140,16 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
 #pragma unroll
   for (int u = 0; u < 2; ++u) {
     int qi = q0 + 16 * u + l16;
-    qi = qi < S ? qi : S - 1;
-    const T* qp = base + static_cast<long long>(qi) * ld + h * HD;
+    qi = qi < Sq ? qi : Sq - 1;
+    const T* qp = static_cast<const T*>(a.q) + (static_cast<long long>(b) * Sq + qi) * a.ldq + h * HD;
 #pragma unroll
     for (int c = 0; c < NC; ++c) qf[u][c] = *reinterpret_cast<const vec*>(qp + 32 * c + 8 * g);
   }
-  const int pad = a.state[kPadAny];
+  const int pad = a.state[a.pad_slot];
   int kend = S;
   if (a.causal) kend = kend < (qb + 1) * kQB ? kend : (qb + 1) * kQB;
   if (pad) {
-    const int kv = a.state[kKvLenBase + b];
+    const int kv = a.state[a.kvlen_base + b];
     kend = kend < kv ? kend : kv;
   }
   const float sl2 = a.scale * 1.4426950408889634f;
@@ -299,9 +301,9 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
 #pragma unroll
   for (int u = 0; u < 2; ++u) {
     const int qi = q0 + 16 * u + l16;
-    if (qi >= S) continue;
+    if (qi >= Sq) continue;
     const float inv = lrow[u] > 0.f ? 1.f / lrow[u] : 0.f;
-    T* out = static_cast<T*>(a.ctx) + (static_cast<long long>(b) * S + qi) * d + h * HD;
+    T* out = static_cast<T*>(a.ctx) + (static_cast<long long>(b) * Sq + qi) * d + h * HD;
 #pragma unroll
     for (int c = 0; c < NCT; ++c) {
       u32x2 r2;
@@ -319,14 +321,14 @@ void attention_force_rows(bool on) { g_attn_rows = on; }
 void launch_attention(const AttnArgs& a, hipStream_t s) {
   const bool mfma_ok = a.dtype != kF32 && (a.hd == 64 || a.hd == 128) && !g_attn_rows;
   if (!mfma_ok) {
-    const dim3 grid(a.S, a.H, a.B);
-    const size_t lds = (a.hd + a.S) * sizeof(float);
+    const dim3 grid(a.Sq, a.H, a.B);
+    const size_t lds = (a.hd + a.Sk) * sizeof(float);
     if (a.dtype == kF32) hipLaunchKernelGGL(k_attn_rows<float>, grid, dim3(64), lds, s, a);
     else if (a.dtype == kBF16) hipLaunchKernelGGL(k_attn_rows<bf16_t>, grid, dim3(64), lds, s, a);
     else hipLaunchKernelGGL(k_attn_rows<f16_t>, grid, dim3(64), lds, s, a);
     return;
   }
-  const dim3 grid((a.S + kQB - 1) / kQB, a.H, a.B);
+  const dim3 grid((a.Sq + kQB - 1) / kQB, a.H, a.B);
   if (a.dtype == kBF16) {
     if (a.hd == 64) hipLaunchKernelGGL((k_attn_mfma<bf16_t, 64>), grid, dim3(256), 0, s, a);
     else hipLaunchKernelGGL((k_attn_mfma<bf16_t, 128>), grid, dim3(256), 0, s, a);

@@ -27,10 +27,13 @@ enum Slot : int {
   kLogCount = 13,    // persistent until flush: log values written to the arena
   kLogDropped = 14,  // persistent until flush: log values lost to overflow
   kRopeLong = 15,    // per-forward: long rotary frequencies selected
-  kClampBase = 16,                    // per-forward: 2*kMaxLayers trip decisions
+  kPadAnyTgt = 16,   // per-forward, encoder-decoder: the target mask has a 0
+  kPadCountTgt = 17, // per-forward, encoder-decoder: number of target mask zeros
+  kClampBase = 32,                    // per-forward: 2*kMaxLayers trip decisions
   kAbsmaxBase = kClampBase + 128,     // per-forward: bits of max |h| per site
   kNanBase = kAbsmaxBase + 128,       // per-forward: NaN seen per site
   kKvLenBase = kNanBase + 128,        // per-forward: 1 + last unmasked key, per sequence
+                                      // (encoder-decoder: the target's follow at + max_batch)
 };
 constexpr int kMaxLayers = 64;
 constexpr uint32_t kTrapNone = 0xFFFFFFFFu;

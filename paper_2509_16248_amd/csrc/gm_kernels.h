@@ -48,12 +48,14 @@ void launch_gemm(const GemmArgs& a, hipStream_t s);
 
 struct AttnArgs {
   int dtype;
-  int B, S, H, hd, d;
-  const void* qkv;          // [B*S, 3d]: q | k | v, head h at columns h*hd
-  void* ctx;                // [B*S, d]
-  const int32_t* mask;      // [B, S]
-  const int32_t* state;     // pad_any flag and kv_len
-  int causal;
+  int B, Sq, Sk, H, hd, d;
+  const void* q; int ldq;   // query (b, i) at row b*Sq + i, head h at columns h*hd
+  const void* k; const void* v; int ldkv;   // key/value (b, j) at row b*Sk + j
+  void* ctx;                // [B*Sq, d]
+  const int32_t* mask;      // [B, Sk] key mask
+  const int32_t* state;     // the padding flag state[pad_slot] and the key
+  int pad_slot, kvlen_base; // lengths state[kvlen_base + b]
+  int causal;               // self-attention only (Sq == Sk): keys j <= i
   float scale;              // 1/sqrt(hd)
 };
 void launch_attention(const AttnArgs& a, hipStream_t s);
@@ -63,11 +65,16 @@ void launch_attention(const AttnArgs& a, hipStream_t s);
 // check of expected against [B, S].  log_vals > 0 zeroes that many floats of
 // log_stage (per-forward tensor log values).  rope_orig > 0: long/short
 // rotary frequency select, long when max(position) + 1 > rope_orig.
+// second != 0: the second input of an encoder-decoder forward (the target):
+// its guards join the trap word already set by the first, with positions
+// offset by index_offset; its padding predicate goes to the target slots and
+// its key lengths to state[kvlen_base + b]; nothing else is touched.
 void launch_prologue(const int32_t* ids, const int32_t* mask, int B, int S,
                      int vocab, int rotary, int capacity, int n_sites,
                      const int32_t* expected, int guard_meta_ok,
                      float* log_stage, int log_vals, int rope_orig,
-                     int32_t* state, hipStream_t s);
+                     int32_t* state, hipStream_t s, int second = 0, int index_offset = 0,
+                     int kvlen_base = 0);
 
 // Tensor-valued log at layer `layer`: stage[layer*B + b] = max |x| over the
 // rows of sequence b of x [B*S, d] (NaN if any element is NaN), as float bits
@@ -101,9 +108,11 @@ void launch_rownorm(const RowArgs& a, hipStream_t s);
 // Effects of a forward in program order: pad, regrow, then per layer the two
 // clamp sites and (n_log_layers > 0) the layer's tensor log of B values,
 // copied from log_stage into the arena (the value at the call site).
+// seq2seq: an encoder-decoder forward, whose source and target padding
+// branches give PAD records with site 0 and 1.
 void launch_emit_effects(int32_t* state, void* fifo, int fifo_cap, int n_sites,
                          const float* log_stage, float* arena, int arena_cap, int n_log_layers,
-                         int B, hipStream_t s);
+                         int B, int seq2seq, hipStream_t s);
 
 // ------------------------------------------------------------ decode step
 // KV cache: per layer, K and V as [max_batch][H][max_seq][hd] (act dtype) and

@@ -29,19 +29,20 @@ __global__ __launch_bounds__(kPrologueThreads) void k_prologue(
     int S, int vocab, int rotary, int capacity, int n_sites,
     const int32_t* __restrict__ expected, int guard_meta_ok,
     float* __restrict__ log_stage, int log_vals, int rope_orig,
-    int32_t* __restrict__ state) {
+    int32_t* __restrict__ state, int pad_slot, int padcount_slot, int kvlen_base,
+    int index_offset, int merge) {
   __shared__ int kv[1024];
   __shared__ uint32_t red_trap[kPrologueThreads / 64];
   __shared__ int red_pad[kPrologueThreads / 64];
   __shared__ int red_need[kPrologueThreads / 64];
   const int tid = threadIdx.x;
   for (int b = tid; b < B; b += blockDim.x) kv[b] = 0;
-  for (int i = tid; i < n_sites; i += blockDim.x) {
+  for (int i = tid; i < (merge ? 0 : n_sites); i += blockDim.x) {
     state[kClampBase + i] = 0;
     state[kAbsmaxBase + i] = 0;
     state[kNanBase + i] = 0;
   }
-  for (int i = tid; i < log_vals; i += blockDim.x) log_stage[i] = 0.f;
+  for (int i = tid; i < (merge ? 0 : log_vals); i += blockDim.x) log_stage[i] = 0.f;
   __syncthreads();
   uint32_t trap = kTrapNone;
   int pads = 0, need = 0;
@@ -50,8 +51,9 @@ __global__ __launch_bounds__(kPrologueThreads) void k_prologue(
     const int id = ids[i];
     const int mk = mask[i];
     const int s = i % S;
-    if (id < 0 || id >= vocab) trap = min(trap, (1u << 24) | static_cast<uint32_t>(i));
-    if (mk != 0 && mk != 1) trap = min(trap, (2u << 24) | static_cast<uint32_t>(i));
+    const uint32_t pos_i = static_cast<uint32_t>(index_offset + i);
+    if (id < 0 || id >= vocab) trap = min(trap, (1u << 24) | pos_i);
+    if (mk != 0 && mk != 1) trap = min(trap, (2u << 24) | pos_i);
     // `if not torch.equal(mask, expected): raise` as (mask == expected).all()
     if (expected && guard_meta_ok && mk != expected[i])
       trap = min(trap, (5u << 24) | static_cast<uint32_t>(i));
@@ -73,8 +75,18 @@ __global__ __launch_bounds__(kPrologueThreads) void k_prologue(
     red_need[w] = need;
   }
   __syncthreads();
-  for (int b = tid; b < B; b += blockDim.x) state[kKvLenBase + b] = kv[b];
-  if (tid == 0) {
+  for (int b = tid; b < B; b += blockDim.x) state[kvlen_base + b] = kv[b];
+  if (tid == 0 && merge) {
+    // second input of an encoder-decoder forward: its guards join the
+    // forward's trap word, its padding predicate gets its own slots
+    for (int i = 1; i < static_cast<int>(blockDim.x >> 6); ++i) {
+      trap = min(trap, red_trap[i]);
+      pads += red_pad[i];
+    }
+    state[kTrapFwd] = static_cast<int32_t>(min(trap, static_cast<uint32_t>(state[kTrapFwd])));
+    state[padcount_slot] = pads;
+    state[pad_slot] = pads > 0;
+  } else if (tid == 0) {
     for (int i = 1; i < static_cast<int>(blockDim.x >> 6); ++i) {
       trap = min(trap, red_trap[i]);
       pads += red_pad[i];
@@ -93,8 +105,10 @@ __global__ __launch_bounds__(kPrologueThreads) void k_prologue(
       state[kCachedLen] = need;
     }
     state[kTrapFwd] = static_cast<int32_t>(trap);
-    state[kPadCount] = pads;
-    state[kPadAny] = pads > 0;
+    state[padcount_slot] = pads;
+    state[pad_slot] = pads > 0;
+    state[kPadAnyTgt] = 0;
+    state[kPadCountTgt] = 0;
     state[kNeed] = need;
     state[kRegrow] = regrow;
     state[kRegrowFrom] = from;
@@ -109,10 +123,15 @@ void launch_prologue(const int32_t* ids, const int32_t* mask, int B, int S,
                      int vocab, int rotary, int capacity, int n_sites,
                      const int32_t* expected, int guard_meta_ok,
                      float* log_stage, int log_vals, int rope_orig,
-                     int32_t* state, hipStream_t s) {
+                     int32_t* state, hipStream_t s, int second, int index_offset,
+                     int kvlen_base) {
+  // the second input (an encoder-decoder's target) has its own padding
+  // slots and key lengths; its positions follow the first input's in the
+  // trap index
   hipLaunchKernelGGL(k_prologue, dim3(1), dim3(kPrologueThreads), 0, s, ids,
                      mask, B, S, vocab, rotary, capacity, n_sites, expected, guard_meta_ok,
-                     log_stage, log_vals, rope_orig, state);
+                     log_stage, log_vals, rope_orig, state, second ? kPadAnyTgt : kPadAny,
+                     second ? kPadCountTgt : kPadCount, kvlen_base, index_offset, second);
 }
 
 // ------------------------------------------------------------ tensor log
@@ -382,7 +401,7 @@ void launch_rownorm(const RowArgs& a, hipStream_t s) {
 __global__ void k_emit_effects(int32_t* __restrict__ state, EffectRec* __restrict__ fifo,
                                int cap, int n_sites, const float* __restrict__ log_stage,
                                float* __restrict__ arena, int arena_cap, int n_log_layers,
-                               int B) {
+                               int B, int seq2seq) {
   if (threadIdx.x != 0) return;
   const int fwd = state[kFwdIndex];
   const uint32_t trap = static_cast<uint32_t>(state[kTrapFwd]);
@@ -410,7 +429,8 @@ __global__ void k_emit_effects(int32_t* __restrict__ state, EffectRec* __restric
       ++dropped;
     }
   };
-  if (state[kPadAny]) push(1, -1, -1, static_cast<float>(state[kPadCount]), 0, 0);
+  if (state[kPadAny]) push(1, -1, seq2seq ? 0 : -1, static_cast<float>(state[kPadCount]), 0, 0);
+  if (seq2seq && state[kPadAnyTgt]) push(1, -1, 1, static_cast<float>(state[kPadCountTgt]), 0, 0);
   if (state[kRegrow]) push(2, -1, -1, static_cast<float>(state[kNeed]), 0, 0);
   const int layers = max(n_sites / 2, n_log_layers);
   for (int l = 0; l < layers; ++l) {
@@ -438,10 +458,11 @@ __global__ void k_emit_effects(int32_t* __restrict__ state, EffectRec* __restric
 }
 
 void launch_emit_effects(int32_t* state, void* fifo, int cap, int n_sites, const float* log_stage,
-                         float* arena, int arena_cap, int n_log_layers, int B, hipStream_t s) {
+                         float* arena, int arena_cap, int n_log_layers, int B, int seq2seq,
+                         hipStream_t s) {
   hipLaunchKernelGGL(k_emit_effects, dim3(1), dim3(64), 0, s, state,
                      static_cast<EffectRec*>(fifo), cap, n_sites, log_stage, arena, arena_cap,
-                     n_log_layers, B);
+                     n_log_layers, B, seq2seq);
 }
 
 // ------------------------------------------------------------ row gather

@@ -48,13 +48,20 @@ struct LayerBufs {
 };
 
 struct GraphEntry {
-  int kind;                 // 0 forward, 1 decode step
+  int kind;                 // 0 forward, 1 decode step, 2 encoder-decoder forward
   int B, S;
   const void *ids, *mask;
   void* logits;
   void* next;
   hipGraphExec_t exec;
   uint64_t last_use;
+  int S2 = 0;               // encoder-decoder: the target's length and inputs
+  const void *ids2 = nullptr, *mask2 = nullptr;
+};
+
+struct CrossBufs {
+  void *lnc_g = nullptr, *lnc_b = nullptr, *wq = nullptr, *bq = nullptr;
+  void *wo = nullptr, *bo = nullptr;
 };
 
 // A decode step's extra launch parameters.
@@ -93,6 +100,8 @@ struct gm_model {
     void* logits;
     std::vector<hipGraphExec_t> execs;
     std::vector<int> kinds;   // what the host reads after segment i (Seg::kinds)
+    int S2 = 0;               // encoder-decoder: the target's length and buffers
+    const void *ids2 = nullptr, *mask2 = nullptr;
   };
   std::vector<Frag> frags;
   bool debug_sync = false;
@@ -106,6 +115,15 @@ struct gm_model {
   float* dpart = nullptr;
   int dec_nsplit = 0;
   int cache_B = 0;          // batch of the last prefill (host-side), 0 = none
+  // encoder-decoder (cfg.n_dec_layers > 0): decoder layers and their
+  // cross-attention, encoder positions and final norm, the encoder output,
+  // the cross queries, and k | v of every decoder layer projected from the
+  // encoder output by one GEMM ([T_src, n_dec * 2d], layer l at l * 2d)
+  std::vector<LayerBufs> dec_layers;
+  std::vector<CrossBufs> dec_cross;
+  void *enc_pos_emb = nullptr, *enc_lnf_g = nullptr, *enc_lnf_b = nullptr;
+  void *wkv_all = nullptr, *bkv_all = nullptr;
+  void *mem = nullptr, *qc = nullptr, *kvc = nullptr;
   // `torch.equal(mask, expected)` guard (gm_set_mask_guard): device tensor and its shape
   const int32_t* guard_expected = nullptr;
   int guard_B = 0, guard_S = 0;
@@ -172,6 +190,16 @@ int validate(const gm_config* c) {
   }
   if (c->rope_scaling != GM_ROPE_PLAIN && c->rope_scaling != GM_ROPE_LONG_SHORT)
     return inval("bad rope_scaling");
+  if (c->n_dec_layers < 0 || c->n_dec_layers > GM_MAX_LAYERS) return inval("n_dec_layers out of [0, 64]");
+  if (c->n_dec_layers) {
+    if (c->norm_place != GM_NORM_PRE || c->pos != GM_POS_LEARNED || !c->causal || c->fp16_clamp ||
+        c->kv_cache || c->log_hidden || c->rope_scaling || c->emb_norm)
+      return inval("encoder-decoder models: pre-norm, learned positions, causal decoder, no "
+                   "fp16_clamp, kv_cache, log_hidden, rope_scaling or emb_norm");
+    if (c->max_tgt < 1) return inval("max_tgt must be positive");
+    if (static_cast<long long>(c->max_batch) * c->max_tgt >= (1ll << 24))
+      return inval("max_batch * max_tgt must be < 2^24");
+  }
   if (c->rope_scaling) {
     if (c->pos != GM_POS_ROTARY) return inval("rope_scaling needs rotary positions");
     if (c->rope_orig_max < 1) return inval("rope_orig_max must be positive");
@@ -282,7 +310,7 @@ struct Seg {
   int cur = 0;
   std::vector<int> kinds;   // what the host reads at each cut (kCut*)
 };
-enum { kCutGuards = 0, kCutClamp = 1000, kCutLog = 2000 };
+enum { kCutGuards = 0, kCutGuardsTgt = 1, kCutClamp = 1000, kCutLog = 2000 };
 constexpr int kCountOnly = -2;
 
 // One forward (dec == null: B x S tokens, with the KV cache filled when the
@@ -318,7 +346,7 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
     launch_prologue(ids, mask, B, S, c.vocab, c.pos == GM_POS_ROTARY, c.rope_capacity, ns,
                     m->guard_expected, m->guard_B == B && m->guard_S == S, m->log_stage,
                     c.log_hidden ? c.n_layers * B : 0,
-                    c.rope_scaling ? c.rope_orig_max : 0, m->state, s);
+                    c.rope_scaling ? c.rope_orig_max : 0, m->state, s, 0, 0, kKvLenBase);
   P(GM_K_PROLOGUE, -1, 0.0, 8.0 * T);
   if (!dec) brk(kCutGuards);  // original program: guards, mask.any() and max(position_ids) read on the host
   if (c.pos == GM_POS_ROTARY && !c.rope_scaling) {
@@ -410,14 +438,20 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
   AttnArgs at{};
   at.dtype = m->dtype;
   at.B = B;
-  at.S = S;
+  at.Sq = at.Sk = S;
   at.H = c.n_heads;
   at.hd = hd;
   at.d = d;
-  at.qkv = m->qkv;
+  at.q = m->qkv;
+  at.ldq = 3 * d;
+  at.k = static_cast<const char*>(m->qkv) + d * m->esz;
+  at.v = static_cast<const char*>(m->qkv) + 2 * d * m->esz;
+  at.ldkv = 3 * d;
   at.ctx = m->ctx;
   at.mask = mask;
   at.state = m->state;
+  at.pad_slot = kPadAny;
+  at.kvlen_base = kKvLenBase;
   at.causal = c.causal;
   at.scale = 1.0f / sqrtf(static_cast<float>(hd));
 
@@ -531,7 +565,185 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
   if (c.kv_cache && on()) launch_seqlen_update(m->seqlen, m->dpos, m->state, B, dec ? 1 : 0, s);
   if (on())
     launch_emit_effects(m->state, m->fifo, kFifoCap, ns, m->log_stage, m->log_arena,
-                        kLogArenaCap, c.log_hidden ? c.n_layers : 0, B, s);
+                        kLogArenaCap, c.log_hidden ? c.n_layers : 0, B, 0, s);
+  P(GM_K_EFFECTS, -1, 0.0, 0.0);
+}
+
+// One encoder-decoder forward: the guards and padding predicates of both
+// inputs, the encoder stack over the source, its final norm (the memory),
+// one GEMM projecting the memory to k | v for every decoder layer, then the
+// decoder stack (causal self-attention under the target's padding branch,
+// cross-attention under the source's) and the head.
+void enqueue_seq2seq(gm_model* m, int B, int Ss, const int32_t* src_ids, const int32_t* src_mask,
+                     int St, const int32_t* tgt_ids, const int32_t* tgt_mask, void* logits,
+                     hipStream_t s, Prof* prof = nullptr, Seg* seg = nullptr) {
+  const gm_config& c = m->cfg;
+  auto on = [&]() { return !seg || seg->want == -1 || seg->want == seg->cur; };
+  auto brk = [&](int kind) {
+    if (seg) {
+      ++seg->cur;
+      seg->kinds.push_back(kind);
+    }
+  };
+  const int d = c.d_model, hd = d / c.n_heads, ff = c.d_ff, nd = c.n_dec_layers;
+  const int Ts = B * Ss, Tt = B * St;
+  const int normk = c.norm == GM_NORM_RMS ? 1 : 0;
+  const double es = static_cast<double>(m->esz);
+  int cur_layer = -1;
+  auto P = [&](int kind, int layer, double flops, double bytes) {
+    if (prof) prof->mark(kind, layer, flops, bytes);
+  };
+  if (prof) prof->start();
+  if (on())
+    launch_prologue(src_ids, src_mask, B, Ss, c.vocab, 0, 0, 0, nullptr, 0, nullptr, 0, 0,
+                    m->state, s, 0, 0, kKvLenBase);
+  P(GM_K_PROLOGUE, -1, 0.0, 8.0 * Ts);
+  brk(kCutGuards);   // original program: the source's guards and mask.any() read on the host
+
+  RowArgs r{};
+  r.dtype = m->dtype;
+  r.d = d;
+  r.eps = c.norm_eps;
+  r.state = m->state;
+  r.clamp_site = -1;
+  r.vocab = c.vocab;
+  r.tok_emb = m->tok_emb;
+  auto embed = [&](int rows, int S, const int32_t* ids, const void* pos) {
+    RowArgs e = r;
+    e.rows = rows;
+    e.ids = ids;
+    e.pos_emb = pos;
+    e.seq = S;
+    e.x = m->h;
+    e.out = m->h;
+    e.norm = -1;
+    if (on()) launch_rownorm(e, s);
+    P(GM_K_EMBED, -1, 0.0, static_cast<double>(rows) * d * es * 3);
+  };
+  auto norm_rows = [&](int rows, void* x, void* out, const void* g, const void* b) {
+    RowArgs q = r;
+    q.rows = rows;
+    q.x = x;
+    q.out = out;
+    q.norm = normk;
+    q.g = g;
+    q.b = b;
+    if (on()) launch_rownorm(q, s);
+    P(GM_K_NORM, cur_layer, 0.0, 2.0 * rows * d * es);
+  };
+  auto gemm = [&](int kind, int M, const void* A, int K, const void* W, int N, int epi,
+                  const void* bias, void* out, int ldo, const void* resid) {
+    GemmArgs q{};
+    q.dtype = m->dtype;
+    q.M = M;
+    q.state = m->state;
+    q.site = -1;
+    q.seq = 1;
+    q.head_dim = hd;
+    q.d_model = d;
+    q.A = A;
+    q.lda = K;
+    q.K = K;
+    q.W = W;
+    q.ldw = K;
+    q.N = N;
+    q.epi = epi;
+    q.bias = bias;
+    q.out = out;
+    q.ldo = ldo;
+    q.resid = resid;
+    q.ldr = ldo;
+    if (on()) launch_gemm(q, s);
+    const int nout = (epi == kEpiGatedGelu || epi == kEpiGatedSilu) ? N / 2 : N;
+    P(kind, cur_layer, 2.0 * M * static_cast<double>(N) * K,
+      es * (static_cast<double>(M) * K + static_cast<double>(N) * K +
+            static_cast<double>(M) * nout * (resid ? 2 : 1)));
+  };
+  AttnArgs at{};
+  at.dtype = m->dtype;
+  at.B = B;
+  at.H = c.n_heads;
+  at.hd = hd;
+  at.d = d;
+  at.ctx = m->ctx;
+  at.state = m->state;
+  at.scale = 1.0f / sqrtf(static_cast<float>(hd));
+  auto attention = [&](int kind, int Sq, int Sk, const void* q, int ldq, const void* k, int ldkv,
+                       const int32_t* mask, int pad_slot, int kv_base, int causal) {
+    AttnArgs a = at;
+    a.Sq = Sq;
+    a.Sk = Sk;
+    a.q = q;
+    a.ldq = ldq;
+    a.k = k;
+    a.v = static_cast<const char*>(k) + d * m->esz;
+    a.ldkv = ldkv;
+    a.mask = mask;
+    a.pad_slot = pad_slot;
+    a.kvlen_base = kv_base;
+    a.causal = causal;
+    if (on()) launch_attention(a, s);
+    const double pairs = causal ? 0.5 * Sq * (Sq + 1.0) : static_cast<double>(Sq) * Sk;
+    P(kind, cur_layer, 4.0 * hd * pairs * B * c.n_heads,
+      es * (static_cast<double>(B) * Sq * 2 * d + static_cast<double>(B) * Sk * 2 * d));
+  };
+  const int up_epi = c.ffn == GM_FFN_GELU ? kEpiGelu
+                     : c.ffn == GM_FFN_GEGLU ? kEpiGatedGelu : kEpiGatedSilu;
+  const int up_n = c.ffn == GM_FFN_GELU ? ff : 2 * ff;
+  char* qkv = static_cast<char*>(m->qkv);
+  auto block_ffn = [&](int rows, const LayerBufs& L) {
+    norm_rows(rows, m->h, m->a, L.ln2_g, L.ln2_b);
+    gemm(GM_K_GEMM_UP, rows, m->a, d, L.w1, up_n, up_epi, L.b1, m->f, ff, nullptr);
+    gemm(GM_K_GEMM_DOWN, rows, m->f, ff, L.w2, d, kEpiResid, L.b2, m->h, d, m->h);
+  };
+
+  // encoder (bidirectional; the source's padding branch)
+  embed(Ts, Ss, src_ids, m->enc_pos_emb);
+  for (int l = 0; l < c.n_layers; ++l) {
+    cur_layer = l;
+    const LayerBufs& L = m->layers[l];
+    norm_rows(Ts, m->h, m->a, L.ln1_g, L.ln1_b);
+    gemm(GM_K_GEMM_QKV, Ts, m->a, d, L.wqkv, 3 * d, kEpiStore, L.bqkv, m->qkv, 3 * d, nullptr);
+    attention(GM_K_ATTENTION, Ss, Ss, qkv, 3 * d, qkv + d * m->esz, 3 * d, src_mask, kPadAny,
+              kKvLenBase, 0);
+    gemm(GM_K_GEMM_O, Ts, m->ctx, d, L.wo, d, kEpiResid, L.bo, m->h, d, m->h);
+    block_ffn(Ts, L);
+  }
+  cur_layer = -1;
+  norm_rows(Ts, m->h, m->mem, m->enc_lnf_g, m->enc_lnf_b);
+  // k | v of every decoder layer from the encoder output, one GEMM
+  gemm(GM_K_GEMM_XKV, Ts, m->mem, d, m->wkv_all, nd * 2 * d, kEpiStore, m->bkv_all, m->kvc,
+       nd * 2 * d, nullptr);
+
+  // decoder (causal self-attention under the target's padding branch,
+  // cross-attention under the source's); its inputs' guards merge into the
+  // forward's trap word
+  if (on())
+    launch_prologue(tgt_ids, tgt_mask, B, St, c.vocab, 0, 0, 0, nullptr, 0, nullptr, 0, 0,
+                    m->state, s, 1, Ts, kKvLenBase + c.max_batch);
+  P(GM_K_PROLOGUE, -1, 0.0, 8.0 * Tt);
+  brk(kCutGuardsTgt);   // original program: the target's guards and mask.any() read on the host
+  embed(Tt, St, tgt_ids, m->pos_emb);
+  for (int l = 0; l < nd; ++l) {
+    cur_layer = c.n_layers + l;
+    const LayerBufs& L = m->dec_layers[l];
+    const CrossBufs& X = m->dec_cross[l];
+    norm_rows(Tt, m->h, m->a, L.ln1_g, L.ln1_b);
+    gemm(GM_K_GEMM_QKV, Tt, m->a, d, L.wqkv, 3 * d, kEpiStore, L.bqkv, m->qkv, 3 * d, nullptr);
+    attention(GM_K_ATTENTION, St, St, qkv, 3 * d, qkv + d * m->esz, 3 * d, tgt_mask, kPadAnyTgt,
+              kKvLenBase + c.max_batch, 1);
+    gemm(GM_K_GEMM_O, Tt, m->ctx, d, L.wo, d, kEpiResid, L.bo, m->h, d, m->h);
+    norm_rows(Tt, m->h, m->a, X.lnc_g, X.lnc_b);
+    gemm(GM_K_GEMM_XQ, Tt, m->a, d, X.wq, d, kEpiStore, X.bq, m->qc, d, nullptr);
+    attention(GM_K_XATTN, St, Ss, m->qc, d, static_cast<char*>(m->kvc) + static_cast<size_t>(l) * 2 * d * m->esz,
+              nd * 2 * d, src_mask, kPadAny, kKvLenBase, 0);
+    gemm(GM_K_GEMM_XO, Tt, m->ctx, d, X.wo, d, kEpiResid, X.bo, m->h, d, m->h);
+    block_ffn(Tt, L);
+  }
+  cur_layer = -1;
+  norm_rows(Tt, m->h, m->a, m->lnf_g, m->lnf_b);
+  gemm(GM_K_GEMM_HEAD, Tt, m->a, d, m->head, c.vocab, kEpiStore, nullptr, logits, c.vocab, nullptr);
+  if (on()) launch_emit_effects(m->state, m->fifo, kFifoCap, 0, nullptr, nullptr, 0, 0, B, 1, s);
   P(GM_K_EFFECTS, -1, 0.0, 0.0);
 }
 
@@ -544,7 +756,8 @@ int launch_graph(gm_model* m, GraphEntry key, hipStream_t stream, Body body) {
   GraphEntry* ge = nullptr;
   for (auto& g : m->graphs)
     if (g.kind == key.kind && g.B == key.B && g.S == key.S && g.ids == key.ids &&
-        g.mask == key.mask && g.logits == key.logits && g.next == key.next)
+        g.mask == key.mask && g.logits == key.logits && g.next == key.next &&
+        g.S2 == key.S2 && g.ids2 == key.ids2 && g.mask2 == key.mask2)
       ge = &g;
   if (!ge) {
     hipGraph_t graph = nullptr;
@@ -635,8 +848,28 @@ int gm_model_create(const gm_config* cfg, const gm_weights* w, gm_model** out) {
       (rc = want(w->lnf_g, pre, "lnf_g")) || (rc = want(w->lnf_b, pre && ln, "lnf_b")) ||
       (rc = want(w->lm_head, !c.tied_head, "lm_head")) ||
       (rc = want(w->rope_short_factor, c.rope_scaling != 0, "rope_short_factor")) ||
-      (rc = want(w->rope_long_factor, c.rope_scaling != 0, "rope_long_factor")))
+      (rc = want(w->rope_long_factor, c.rope_scaling != 0, "rope_long_factor")) ||
+      (rc = want(w->enc_pos_emb, c.n_dec_layers > 0, "enc_pos_emb")) ||
+      (rc = want(w->enc_lnf_g, c.n_dec_layers > 0, "enc_lnf_g")) ||
+      (rc = want(w->enc_lnf_b, c.n_dec_layers > 0 && ln, "enc_lnf_b")) ||
+      (rc = want(w->dec_layers, c.n_dec_layers > 0, "dec_layers")) ||
+      (rc = want(w->dec_cross, c.n_dec_layers > 0, "dec_cross")))
     return rc;
+  for (int l = 0; l < c.n_dec_layers; ++l) {
+    const gm_layer_weights& L = w->dec_layers[l];
+    const gm_cross_weights& X = w->dec_cross[l];
+    if ((rc = want(L.ln1_g, true, "dec ln1_g")) || (rc = want(L.ln1_b, ln, "dec ln1_b")) ||
+        (rc = want(L.ln2_g, true, "dec ln2_g")) || (rc = want(L.ln2_b, ln, "dec ln2_b")) ||
+        (rc = want(L.wqkv, true, "dec wqkv")) || (rc = want(L.wo, true, "dec wo")) ||
+        (rc = want(L.w1, true, "dec w1")) || (rc = want(L.w2, true, "dec w2")) ||
+        (rc = want(L.bqkv, c.has_bias, "dec bqkv")) || (rc = want(L.bo, c.has_bias, "dec bo")) ||
+        (rc = want(L.b1, c.has_bias, "dec b1")) || (rc = want(L.b2, c.has_bias, "dec b2")) ||
+        (rc = want(X.lnc_g, true, "lnc_g")) || (rc = want(X.lnc_b, ln, "lnc_b")) ||
+        (rc = want(X.wq, true, "cross wq")) || (rc = want(X.wkv, true, "cross wkv")) ||
+        (rc = want(X.wo, true, "cross wo")) || (rc = want(X.bq, c.has_bias, "cross bq")) ||
+        (rc = want(X.bkv, c.has_bias, "cross bkv")) || (rc = want(X.bo, c.has_bias, "cross bo")))
+      return rc;
+  }
   for (int l = 0; l < c.n_layers; ++l) {
     const gm_layer_weights& L = w->layers[l];
     if ((rc = want(L.ln1_g, true, "ln1_g")) || (rc = want(L.ln1_b, ln, "ln1_b")) ||
@@ -672,8 +905,60 @@ int gm_model_create(const gm_config* cfg, const gm_weights* w, gm_model** out) {
   const std::vector<int32_t>* rpp = c.pos == GM_POS_ROTARY ? &rp : nullptr;
 
   if ((rc = copy_in(m, &m->tok_emb, w->tok_emb, V, d, nullptr, "tok_emb"))) return fail(rc);
-  if (c.pos == GM_POS_LEARNED && (rc = copy_in(m, &m->pos_emb, w->pos_emb, c.max_seq, d, nullptr, "pos_emb")))
+  // learned positions: max_seq rows (an encoder-decoder's decoder: max_tgt)
+  if (c.pos == GM_POS_LEARNED &&
+      (rc = copy_in(m, &m->pos_emb, w->pos_emb, c.n_dec_layers ? c.max_tgt : c.max_seq, d, nullptr,
+                    "pos_emb")))
     return fail(rc);
+  if (c.n_dec_layers) {
+    if ((rc = copy_in(m, &m->enc_pos_emb, w->enc_pos_emb, c.max_seq, d, nullptr, "enc_pos_emb")) ||
+        (rc = copy_in(m, &m->enc_lnf_g, w->enc_lnf_g, 1, d, nullptr, "enc_lnf_g")) ||
+        (ln && (rc = copy_in(m, &m->enc_lnf_b, w->enc_lnf_b, 1, d, nullptr, "enc_lnf_b"))))
+      return fail(rc);
+    const int nd = c.n_dec_layers;
+    m->dec_layers.resize(nd);
+    m->dec_cross.resize(nd);
+    // k | v projections of all decoder layers, stacked: one GEMM over the
+    // encoder output serves every layer's cross-attention
+    const size_t kv_rows = static_cast<size_t>(2) * d;
+    const size_t kv_bytes = kv_rows * d * m->esz;
+    if ((rc = m->alloc(&m->wkv_all, nd * kv_bytes))) return fail(rc);
+    if (c.has_bias && (rc = m->alloc(&m->bkv_all, nd * kv_rows * m->esz))) return fail(rc);
+    for (int l = 0; l < nd; ++l) {
+      const gm_layer_weights& L = w->dec_layers[l];
+      const gm_cross_weights& X = w->dec_cross[l];
+      LayerBufs& D = m->dec_layers[l];
+      CrossBufs& C = m->dec_cross[l];
+      if ((rc = copy_in(m, &D.ln1_g, L.ln1_g, 1, d, nullptr, "dec ln1_g")) ||
+          (ln && (rc = copy_in(m, &D.ln1_b, L.ln1_b, 1, d, nullptr, "dec ln1_b"))) ||
+          (rc = copy_in(m, &D.ln2_g, L.ln2_g, 1, d, nullptr, "dec ln2_g")) ||
+          (ln && (rc = copy_in(m, &D.ln2_b, L.ln2_b, 1, d, nullptr, "dec ln2_b"))) ||
+          (rc = copy_in(m, &D.wqkv, L.wqkv, 3 * d, d, nullptr, "dec wqkv")) ||
+          (rc = copy_in(m, &D.wo, L.wo, d, d, nullptr, "dec wo")) ||
+          (rc = copy_in(m, &D.w1, L.w1, gated ? 2 * ff : ff, d, gpp, "dec w1")) ||
+          (rc = copy_in(m, &D.w2, L.w2, d, ff, nullptr, "dec w2")) ||
+          (rc = copy_in(m, &C.lnc_g, X.lnc_g, 1, d, nullptr, "lnc_g")) ||
+          (ln && (rc = copy_in(m, &C.lnc_b, X.lnc_b, 1, d, nullptr, "lnc_b"))) ||
+          (rc = copy_in(m, &C.wq, X.wq, d, d, nullptr, "cross wq")) ||
+          (rc = copy_in(m, &C.wo, X.wo, d, d, nullptr, "cross wo")))
+        return fail(rc);
+      e = hipMemcpy(static_cast<char*>(m->wkv_all) + l * kv_bytes, X.wkv, kv_bytes,
+                    hipMemcpyDeviceToDevice);
+      if (e != hipSuccess) return fail(hip_fail(e, "cross wkv"));
+      if (c.has_bias) {
+        if ((rc = copy_in(m, &D.bqkv, L.bqkv, 3 * d, 1, nullptr, "dec bqkv")) ||
+            (rc = copy_in(m, &D.bo, L.bo, d, 1, nullptr, "dec bo")) ||
+            (rc = copy_in(m, &D.b1, L.b1, gated ? 2 * ff : ff, 1, gpp, "dec b1")) ||
+            (rc = copy_in(m, &D.b2, L.b2, d, 1, nullptr, "dec b2")) ||
+            (rc = copy_in(m, &C.bq, X.bq, d, 1, nullptr, "cross bq")) ||
+            (rc = copy_in(m, &C.bo, X.bo, d, 1, nullptr, "cross bo")))
+          return fail(rc);
+        e = hipMemcpy(static_cast<char*>(m->bkv_all) + l * kv_rows * m->esz, X.bkv,
+                      kv_rows * m->esz, hipMemcpyDeviceToDevice);
+        if (e != hipSuccess) return fail(hip_fail(e, "cross bkv"));
+      }
+    }
+  }
   if (c.emb_norm) {
     if ((rc = copy_in(m, &m->emb_ln_g, w->emb_ln_g, 1, d, nullptr, "emb_ln_g"))) return fail(rc);
     if (ln && (rc = copy_in(m, &m->emb_ln_b, w->emb_ln_b, 1, d, nullptr, "emb_ln_b"))) return fail(rc);
@@ -708,9 +993,17 @@ int gm_model_create(const gm_config* cfg, const gm_weights* w, gm_model** out) {
     }
   }
 
-  // workspace
-  const size_t T = static_cast<size_t>(c.max_batch) * c.max_seq;
+  // workspace (an encoder-decoder's decoder reuses it for max_tgt positions)
+  const size_t T = static_cast<size_t>(c.max_batch) *
+                   (c.n_dec_layers && c.max_tgt > c.max_seq ? c.max_tgt : c.max_seq);
   const size_t es = m->esz;
+  if (c.n_dec_layers) {
+    const size_t Ts = static_cast<size_t>(c.max_batch) * c.max_seq;
+    const size_t Tt = static_cast<size_t>(c.max_batch) * c.max_tgt;
+    if ((rc = m->alloc(&m->mem, Ts * d * es)) || (rc = m->alloc(&m->qc, Tt * d * es)) ||
+        (rc = m->alloc(&m->kvc, Ts * c.n_dec_layers * 2 * d * es)))
+      return fail(rc);
+  }
   if ((rc = m->alloc(&m->h, T * d * es)) || (rc = m->alloc(&m->a, T * d * es)) ||
       (rc = m->alloc(&m->qkv, T * 3 * d * es)) || (rc = m->alloc(&m->ctx, T * d * es)) ||
       (rc = m->alloc(&m->f, T * ff * es)) ||
@@ -741,8 +1034,8 @@ int gm_model_create(const gm_config* cfg, const gm_weights* w, gm_model** out) {
     if (e == hipSuccess) e = hipMemset(m->dpos, 0, c.max_batch * sizeof(int32_t));
     if (e != hipSuccess) return fail(hip_fail(e, "hipMemset"));
   }
-  // device state
-  m->n_state = kKvLenBase + c.max_batch;
+  // device state (encoder-decoder: the target's key lengths follow the source's)
+  m->n_state = kKvLenBase + 2 * c.max_batch;
   void* p = nullptr;
   if ((rc = m->alloc(&p, m->n_state * sizeof(int32_t)))) return fail(rc);
   m->state = static_cast<int32_t*>(p);
@@ -817,27 +1110,36 @@ int gm_set_graph_mode(gm_model* m, int32_t enabled) {
   return gm_set_exec_mode(m, enabled ? GM_EXEC_GRAPH : GM_EXEC_EAGER);
 }
 
+}  // extern "C"
+
 // The unmended program: every data-dependent branch is a host decision.  Each
 // stretch between two such reads is one captured graph (one per fused
 // region, as the paper's baseline captures them); at each cut the host
 // synchronises the stream, copies the predicate's inputs back and evaluates
 // the branch.  The kernels are the same as in the single-graph forward.
-static int forward_fragmented(gm_model* m, int B, int S, const int32_t* ids,
-                              const int32_t* mask, void* logits, hipStream_t stream) {
+// `key` names the forward (shape and buffers); body(stream, seg) enqueues it.
+template <typename Body>
+static int forward_fragmented(gm_model* m, const gm_model::Frag& key, hipStream_t stream,
+                              Body body) {
+  const int B = key.B;
   gm_model::Frag* fr = nullptr;
   for (auto& f : m->frags)
-    if (f.B == B && f.S == S && f.ids == ids && f.mask == mask && f.logits == logits) fr = &f;
+    if (f.B == B && f.S == key.S && f.ids == key.ids && f.mask == key.mask &&
+        f.logits == key.logits && f.S2 == key.S2 && f.ids2 == key.ids2 && f.mask2 == key.mask2)
+      fr = &f;
   if (!fr) {
     Seg count;
     count.want = kCountOnly;
-    enqueue(m, B, S, ids, mask, logits, m->cap_stream, nullptr, &count);
-    gm_model::Frag f{B, S, ids, mask, logits, {}, count.kinds};
+    body(m->cap_stream, &count);
+    gm_model::Frag f = key;
+    f.execs.clear();
+    f.kinds = count.kinds;
     for (int i = 0; i <= count.cur; ++i) {
       hipGraph_t graph = nullptr;
       HIP_TRY(hipStreamBeginCapture(m->cap_stream, hipStreamCaptureModeThreadLocal));
       Seg sg;
       sg.want = i;
-      enqueue(m, B, S, ids, mask, logits, m->cap_stream, nullptr, &sg);
+      body(m->cap_stream, &sg);
       hipError_t e = hipStreamEndCapture(m->cap_stream, &graph);
       if (e != hipSuccess || !graph) {
         g_last_error = std::string("capture: ") + hipGetErrorString(e);
@@ -869,7 +1171,7 @@ static int forward_fragmented(gm_model* m, int B, int S, const int32_t* ids,
     m->stats.host_syncs_in_forward++;
     HIP_TRY(hipStreamSynchronize(stream));
     const int kind = fr->kinds[i];
-    if (kind == kCutGuards) {
+    if (kind == kCutGuards || kind == kCutGuardsTgt) {
       HIP_TRY(hipMemcpy(host, m->state, sizeof(int32_t) * kClampBase, hipMemcpyDeviceToHost));
       const uint32_t trap = static_cast<uint32_t>(host[kTrapFwd]);
       if (trap != kTrapNone) {  // `if not C: raise` -- the forward stops at the guard
@@ -882,7 +1184,7 @@ static int forward_fragmented(gm_model* m, int B, int S, const int32_t* ids,
         g_last_error = "input guard failed (fragmented execution stops at the guard)";
         return GM_E_TRAP;
       }
-      m->last_host_pad_any = host[kPadAny] != 0;      // `if mask.any():`
+      m->last_host_pad_any = host[kind == kCutGuards ? kPadAny : kPadAnyTgt] != 0;  // `if mask.any():`
       m->last_host_regrow = host[kRegrow] != 0;       // `if seq_len > cached:`
     } else if (kind >= kCutLog) {
       // `logger.info(..., tensor)`: the values come back to the host to be printed
@@ -905,6 +1207,8 @@ static int forward_fragmented(gm_model* m, int B, int S, const int32_t* ids,
   return GM_OK;
 }
 
+extern "C" {
+
 int gm_forward_ex(gm_model* m, int32_t B, int32_t S, const int32_t* ids, const int32_t* mask,
                   void* logits, hipStream_t stream) {
   if (!m) return inval("model is NULL");
@@ -914,9 +1218,14 @@ int gm_forward_ex(gm_model* m, int32_t B, int32_t S, const int32_t* ids, const i
     return inval("ids, mask and logits must be 16-byte aligned");
   if (B < 1 || B > m->cfg.max_batch || S < 1 || S > m->cfg.max_seq)
     return inval("B or S out of range");
+  if (m->cfg.n_dec_layers) return inval("an encoder-decoder model runs gm_forward_seq2seq");
   m->stats.forwards++;
   if (m->cfg.kv_cache) m->cache_B = B;   // the forward fills the cache for these B sequences
-  if (m->exec_mode == GM_EXEC_FRAGMENTED) return forward_fragmented(m, B, S, ids, mask, logits, stream);
+  if (m->exec_mode == GM_EXEC_FRAGMENTED)
+    return forward_fragmented(m, gm_model::Frag{B, S, ids, mask, logits, {}, {}}, stream,
+                              [&](hipStream_t cs, Seg* sg) {
+                                enqueue(m, B, S, ids, mask, logits, cs, nullptr, sg);
+                              });
   if (m->exec_mode == GM_EXEC_EAGER) {
     enqueue(m, B, S, ids, mask, logits, stream);
     HIP_TRY(hipGetLastError());
@@ -929,6 +1238,45 @@ int gm_forward_ex(gm_model* m, int32_t B, int32_t S, const int32_t* ids, const i
   }
   return launch_graph(m, GraphEntry{0, B, S, ids, mask, logits, nullptr, nullptr, 0}, stream,
                       [&](hipStream_t cs) { enqueue(m, B, S, ids, mask, logits, cs); });
+}
+
+int gm_forward_seq2seq(gm_model* m, int32_t B, int32_t Ss, const int32_t* src_ids,
+                       const int32_t* src_mask, int32_t St, const int32_t* tgt_ids,
+                       const int32_t* tgt_mask, void* logits, hipStream_t stream) {
+  if (!m) return inval("model is NULL");
+  if (!m->cfg.n_dec_layers) return inval("not an encoder-decoder model (n_dec_layers == 0)");
+  if (!src_ids || !src_mask || !tgt_ids || !tgt_mask || !logits)
+    return inval("inputs and logits must be non-NULL");
+  if ((reinterpret_cast<uintptr_t>(src_ids) | reinterpret_cast<uintptr_t>(src_mask) |
+       reinterpret_cast<uintptr_t>(tgt_ids) | reinterpret_cast<uintptr_t>(tgt_mask) |
+       reinterpret_cast<uintptr_t>(logits)) & 15)
+    return inval("inputs and logits must be 16-byte aligned");
+  if (B < 1 || B > m->cfg.max_batch || Ss < 1 || Ss > m->cfg.max_seq || St < 1 ||
+      St > m->cfg.max_tgt)
+    return inval("B, S_src or S_tgt out of range");
+  m->stats.forwards++;
+  if (m->exec_mode == GM_EXEC_FRAGMENTED) {
+    gm_model::Frag key{B, Ss, src_ids, src_mask, logits, {}, {}};
+    key.S2 = St;
+    key.ids2 = tgt_ids;
+    key.mask2 = tgt_mask;
+    return forward_fragmented(m, key, stream, [&](hipStream_t cs, Seg* sg) {
+      enqueue_seq2seq(m, B, Ss, src_ids, src_mask, St, tgt_ids, tgt_mask, logits, cs, nullptr, sg);
+    });
+  }
+  if (m->exec_mode == GM_EXEC_EAGER) {
+    enqueue_seq2seq(m, B, Ss, src_ids, src_mask, St, tgt_ids, tgt_mask, logits, stream);
+    HIP_TRY(hipGetLastError());
+    m->stats.eager_forwards++;
+    return GM_OK;
+  }
+  GraphEntry key{2, B, Ss, src_ids, src_mask, logits, nullptr, nullptr, 0};
+  key.S2 = St;
+  key.ids2 = tgt_ids;
+  key.mask2 = tgt_mask;
+  return launch_graph(m, key, stream, [&](hipStream_t cs) {
+    enqueue_seq2seq(m, B, Ss, src_ids, src_mask, St, tgt_ids, tgt_mask, logits, cs);
+  });
 }
 
 int gm_decode_step(gm_model* m, int32_t B, const int32_t* ids, void* logits, int32_t* next,
@@ -963,6 +1311,7 @@ int gm_profile_forward(gm_model* m, int32_t B, int32_t S, const int32_t* ids,
                        const int32_t* mask, void* logits, hipStream_t stream,
                        gm_kernel_time* out, int32_t cap, int32_t* n_out) {
   if (!m || !out || !n_out) return inval("NULL argument");
+  if (m->cfg.n_dec_layers) return inval("profiling covers decoder-only and encoder-only forwards");
   if (!ids || !mask || !logits) return inval("ids, mask and logits must be non-NULL");
   if ((reinterpret_cast<uintptr_t>(ids) | reinterpret_cast<uintptr_t>(mask) |
        reinterpret_cast<uintptr_t>(logits)) & 15)
@@ -1016,6 +1365,7 @@ int gm_read_decisions(gm_model* m, gm_decisions* out, hipStream_t stream) {
   }
   out->forward_index = st[kFwdIndex];
   out->rope_long = st[kRopeLong];
+  out->pad_any_tgt = st[kPadAnyTgt];
   return GM_OK;
 }
 

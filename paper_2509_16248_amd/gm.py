@@ -40,7 +40,8 @@ class gm_config(ctypes.Structure):
                 ("rope_init_len", _i32), ("rope_capacity", _i32),
                 ("act_dtype", _i32), ("fp16_clamp", _i32), ("clamp_margin", _f32),
                 ("kv_cache", _i32), ("log_hidden", _i32), ("rope_scaling", _i32),
-                ("rope_orig_max", _i32), ("rope_attn_factor", _f32)]
+                ("rope_orig_max", _i32), ("rope_attn_factor", _f32),
+                ("n_dec_layers", _i32), ("max_tgt", _i32)]
 
 
 LAYER_FIELDS = ["ln1_g", "ln1_b", "wqkv", "bqkv", "wo", "bo", "ln2_g", "ln2_b",
@@ -52,9 +53,19 @@ class gm_layer_weights(ctypes.Structure):
     _fields_ = [(n, _vp) for n in LAYER_FIELDS]
 
 
+CROSS_FIELDS = ["lnc_g", "lnc_b", "wq", "bq", "wkv", "bkv", "wo", "bo"]
+
+
+class gm_cross_weights(ctypes.Structure):
+    _fields_ = [(n, _vp) for n in CROSS_FIELDS]
+
+
 class gm_weights(ctypes.Structure):
     _fields_ = ([(n, _vp) for n in GLOBAL_FIELDS] + [("layers", ctypes.POINTER(gm_layer_weights))]
-                + [("rope_short_factor", _vp), ("rope_long_factor", _vp)])
+                + [("rope_short_factor", _vp), ("rope_long_factor", _vp),
+                   ("enc_pos_emb", _vp), ("enc_lnf_g", _vp), ("enc_lnf_b", _vp),
+                   ("dec_layers", ctypes.POINTER(gm_layer_weights)),
+                   ("dec_cross", ctypes.POINTER(gm_cross_weights))])
 
 
 class gm_decisions(ctypes.Structure):
@@ -63,7 +74,7 @@ class gm_decisions(ctypes.Structure):
                 ("clamp", _i32 * (2 * GM_MAX_LAYERS)),
                 ("clamp_absmax", _f32 * (2 * GM_MAX_LAYERS)),
                 ("clamp_nan", _i32 * (2 * GM_MAX_LAYERS)),
-                ("forward_index", _i32), ("rope_long", _i32)]
+                ("forward_index", _i32), ("rope_long", _i32), ("pad_any_tgt", _i32)]
 
 
 class gm_effect(ctypes.Structure):
@@ -85,12 +96,12 @@ class gm_kernel_time(ctypes.Structure):
 
 KERNEL_KINDS = ["prologue", "rope_fill", "embed", "norm", "gemm_qkv", "attention",
                 "gemm_o", "gemm_up", "gemm_down", "gemm_head", "effects", "kv_store",
-                "argmax", "log"]
+                "argmax", "log", "gemm_xq", "gemm_xkv", "gemm_xo", "xattn"]
 
 gm_effect_cb = ctypes.CFUNCTYPE(None, ctypes.POINTER(gm_effect), ctypes.c_void_p)
 
 EXPORTS = ["gm_model_create", "gm_model_destroy", "gm_forward", "gm_forward_ex",
-           "gm_decode_step", "gm_set_mask_guard", "gm_trap_info",
+           "gm_decode_step", "gm_set_mask_guard", "gm_trap_info", "gm_forward_seq2seq",
            "gm_profile_forward", "gm_set_exec_mode", "gm_set_graph_mode", "gm_read_decisions", "gm_decisions_device_ptr",
            "gm_check_error", "gm_flush_effects", "gm_debug_buffer", "gm_get_stats",
            "gm_strerror",
@@ -116,6 +127,7 @@ def lib(path: str = LIB_PATH) -> ctypes.CDLL:
     L.gm_forward_ex.argtypes = [_vp, _i32, _i32, _vp, _vp, _vp, _vp]
     L.gm_decode_step.argtypes = [_vp, _i32, _vp, _vp, _vp, _vp]
     L.gm_set_mask_guard.argtypes = [_vp, _vp, _i32, _i32]
+    L.gm_forward_seq2seq.argtypes = [_vp, _i32, _i32, _vp, _vp, _i32, _vp, _vp, _vp, _vp]
     L.gm_trap_info.argtypes = [_i32, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_char_p)]
     L.gm_set_graph_mode.argtypes = [_vp, _i32]
     L.gm_set_exec_mode.argtypes = [_vp, _i32]
@@ -177,6 +189,12 @@ def gm_forward_ex(m: int, B: int, S: int, ids: int, mask: int, logits: int, stre
 def gm_decode_step(m: int, B: int, ids: int, logits: int, next_ids: Optional[int],
                    stream: int) -> None:
     _check(lib().gm_decode_step(m, B, ids, logits, next_ids, stream), "gm_decode_step")
+
+
+def gm_forward_seq2seq(m: int, B: int, S_src: int, src_ids: int, src_mask: int, S_tgt: int,
+                       tgt_ids: int, tgt_mask: int, logits: int, stream: int) -> None:
+    _check(lib().gm_forward_seq2seq(m, B, S_src, src_ids, src_mask, S_tgt, tgt_ids, tgt_mask,
+                                    logits, stream), "gm_forward_seq2seq")
 
 
 def gm_set_mask_guard(m: int, expected: Optional[int], B: int, S: int) -> None:

@@ -39,7 +39,9 @@ def make_config(c, max_batch: Optional[int] = None, max_seq: Optional[int] = Non
         rope_scaling={"none": gm.GM_ROPE_PLAIN, "long_short": gm.GM_ROPE_LONG_SHORT}[
             getattr(c, "rope_scaling", "none")],
         rope_orig_max=int(getattr(c, "rope_orig_max", 0)),
-        rope_attn_factor=float(getattr(c, "rope_attn_factor", 1.0)))
+        rope_attn_factor=float(getattr(c, "rope_attn_factor", 1.0)),
+        n_dec_layers=int(getattr(c, "n_dec_layers", 0)),
+        max_tgt=int(getattr(c, "tgt_seq", 0)))
 
 
 def to_device(a: np.ndarray, dtype: str, device) -> torch.Tensor:
@@ -59,7 +61,7 @@ class GmModel:
 
     def __init__(self, cfg, globals_: Dict, layers: List[Dict], device="cuda",
                  max_batch: Optional[int] = None, max_seq: Optional[int] = None,
-                 kv_cache: bool = False):
+                 kv_cache: bool = False, dec_layers: Optional[List[Dict]] = None):
         self.cfg = cfg
         self.device = torch.device(device)
         self.c = make_config(cfg, max_batch, max_seq, kv_cache)
@@ -85,6 +87,25 @@ class GmModel:
                 keep.append(t)
                 setattr(arr[l], name, t.data_ptr() if t is not None else None)
         w.layers = ctypes.cast(arr, ctypes.POINTER(gm.gm_layer_weights))
+        for name in ("enc_pos_emb", "enc_lnf_g", "enc_lnf_b"):
+            t = dev(globals_.get(name))
+            keep.append(t)
+            setattr(w, name, t.data_ptr() if t is not None else None)
+        if dec_layers:
+            darr = (gm.gm_layer_weights * len(dec_layers))()
+            xarr = (gm.gm_cross_weights * len(dec_layers))()
+            for l, L in enumerate(dec_layers):
+                for name in gm.LAYER_FIELDS:
+                    t = dev(L.get(name))
+                    keep.append(t)
+                    setattr(darr[l], name, t.data_ptr() if t is not None else None)
+                for name in gm.CROSS_FIELDS:
+                    t = dev(L.get("x_" + name))
+                    keep.append(t)
+                    setattr(xarr[l], name, t.data_ptr() if t is not None else None)
+            keep += [darr, xarr]
+            w.dec_layers = ctypes.cast(darr, ctypes.POINTER(gm.gm_layer_weights))
+            w.dec_cross = ctypes.cast(xarr, ctypes.POINTER(gm.gm_cross_weights))
         for name in ("rope_short_factor", "rope_long_factor"):
             x = globals_.get(name)
             if x is not None:
@@ -109,6 +130,21 @@ class GmModel:
         assert logits.dtype == _TORCH[self.cfg.dtype]
         gm.gm_forward_ex(self.handle, B, S, ids.data_ptr(), mask.data_ptr(),
                          logits.data_ptr(), self._stream(stream))
+        return logits
+
+    def forward_seq2seq(self, src_ids: torch.Tensor, src_mask: torch.Tensor,
+                        tgt_ids: torch.Tensor, tgt_mask: torch.Tensor, logits: torch.Tensor,
+                        stream=None) -> torch.Tensor:
+        """Encoder-decoder forward (gm_forward_seq2seq): logits [B, S_tgt, V]."""
+        B, Ss = src_ids.shape
+        St = tgt_ids.shape[1]
+        for t in (src_ids, src_mask, tgt_ids, tgt_mask):
+            assert t.dtype == torch.int32 and t.is_contiguous()
+        assert src_mask.shape == (B, Ss) and tgt_ids.shape == tgt_mask.shape == (B, St)
+        assert logits.shape == (B, St, self.c.vocab) and logits.is_contiguous()
+        gm.gm_forward_seq2seq(self.handle, B, Ss, src_ids.data_ptr(), src_mask.data_ptr(), St,
+                              tgt_ids.data_ptr(), tgt_mask.data_ptr(), logits.data_ptr(),
+                              self._stream(stream))
         return logits
 
     def decode(self, ids: torch.Tensor, logits: torch.Tensor,
@@ -156,7 +192,7 @@ class GmModel:
                 "clamp": [bool(d.clamp[i]) for i in range(n)],
                 "clamp_absmax": [d.clamp_absmax[i] for i in range(n)],
                 "clamp_nan": [bool(d.clamp_nan[i]) for i in range(n)],
-                "rope_long": bool(d.rope_long)}
+                "rope_long": bool(d.rope_long), "pad_any_tgt": bool(d.pad_any_tgt)}
 
     def check_error(self):
         return gm.gm_check_error(self.handle)

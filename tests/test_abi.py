@@ -15,7 +15,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 def declared_functions():
     src = open(os.path.join(ROOT, "include", "gm.h")).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    names = re.findall(r"\b(gm_[a-z_]+)\s*\(", src)
+    names = re.findall(r"\b(gm_[a-z0-9_]+)\s*\(", src)
     return sorted(set(n for n in names if not n.endswith("_cb")))
 
 
