@@ -264,6 +264,8 @@ def main():
     ap.add_argument("--no-decode", action="store_true", help="skip the KV-cache decode measurement")
     ap.add_argument("--no-seq2seq", action="store_true",
                     help="skip the encoder-decoder measurement")
+    ap.add_argument("--seq2seq-only", action="store_true",
+                    help="only the encoder-decoder measurement (one JSON object)")
     ap.add_argument("--break-suite", action="store_true",
                     help="only compare single-graph and graph-broken forwards on every workload")
     args = ap.parse_args()
@@ -280,6 +282,9 @@ def main():
 
     if args.break_suite:
         break_suite(args)
+        return
+    if args.seq2seq_only:
+        print(json.dumps(seq2seq_bench(args)), flush=True)
         return
     cfg = synth.preset(WORKLOAD)
     B, S = cfg.batch, cfg.seq

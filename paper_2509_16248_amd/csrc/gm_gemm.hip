@@ -733,8 +733,12 @@ static void gemm_mfma(const GemmArgs& a, hipStream_t s, int variant) {
   }
   // 128 x 128 workgroup tiles, 8 wavefronts of 64 x 32, operands fetched two
   // K steps ahead (the best of the measured configurations on the projection
-  // and head shapes)
-  run_x<T, 128, 128, 2, 4, 2>(a, s);
+  // and head shapes).  Products too small to give the chip ~160 such tiles
+  // (1024-row decoder GEMMs of an encoder-decoder: N 768 gives 48) take
+  // 64 x 64 tiles on 4 wavefronts of 32 x 32: four times the workgroups.
+  const long long tiles128 = ((a.M + 127) / 128) * static_cast<long long>((a.N + 127) / 128);
+  if (tiles128 < 160) run_x<T, 64, 64, 2, 2, 2>(a, s);
+  else run_x<T, 128, 128, 2, 4, 2>(a, s);
 }
 
 // ------------------------------------------------------------ fp32 kernel
