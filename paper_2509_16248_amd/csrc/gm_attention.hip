@@ -104,15 +104,17 @@ template <> struct MfmaA<f16_t> {
   }
 };
 
-constexpr int kQB = 128, kKB = 64;
+constexpr int kKB = 64;
 
 // K and V tiles move global -> registers -> LDS.  The tile after the current
 // one is fetched into registers while the current one is multiplied, and the
 // LDS tiles are double-buffered, so there is one barrier per key tile.  V is
 // transposed on the way into LDS, two keys at a time (4-byte LDS writes).
-// With a causal mask, query blocks run heaviest (last) first.
-template <typename T, int HD>
+// With a causal mask, query blocks run heaviest (last) first.  A wavefront
+// holds 16 U queries (U = 1: 64 queries per workgroup).
+template <typename T, int HD, int U>
 __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
+  constexpr int QB = 64 * U;       // queries per workgroup: 4 wavefronts x 16U
   typedef typename MfmaA<T>::vec vec;
   constexpr int LDK = HD + 8;      // K tile row pitch (elements)
   constexpr int LDV = kKB + 4;     // V^T tile row pitch (transposing writes spread over banks)
@@ -125,7 +127,7 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) T sK[2][kKB * LDK];
   __shared__ __attribute__((aligned(16))) T sVt[2][HD * LDV];
   __shared__ int sMask[2][kKB];
-  const int nqb = (a.Sq + kQB - 1) / kQB;
+  const int nqb = (a.Sq + QB - 1) / QB;
   const int qb = a.causal ? nqb - 1 - static_cast<int>(blockIdx.x) : static_cast<int>(blockIdx.x);
   const int h = blockIdx.y, b = blockIdx.z;
   const int Sq = a.Sq, S = a.Sk, d = a.d, ld = a.ldkv;
@@ -134,11 +136,11 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
   const T* kbase = static_cast<const T*>(a.k) + static_cast<long long>(b) * S * ld + h * HD;
   const T* vbase = static_cast<const T*>(a.v) + static_cast<long long>(b) * S * ld + h * HD;
   const int32_t* mk = a.mask + static_cast<long long>(b) * S;
-  const int q0 = qb * kQB + wave * 32;
+  const int q0 = qb * QB + wave * 16 * U;
 
-  vec qf[2][NC];
+  vec qf[U][NC];
 #pragma unroll
-  for (int u = 0; u < 2; ++u) {
+  for (int u = 0; u < U; ++u) {
     int qi = q0 + 16 * u + l16;
     qi = qi < Sq ? qi : Sq - 1;
     const T* qp = static_cast<const T*>(a.q) + (static_cast<long long>(b) * Sq + qi) * a.ldq + h * HD;
@@ -147,17 +149,22 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
   }
   const int pad = a.state[a.pad_slot];
   int kend = S;
-  if (a.causal) kend = kend < (qb + 1) * kQB ? kend : (qb + 1) * kQB;
+  if (a.causal) kend = kend < (qb + 1) * QB ? kend : (qb + 1) * QB;
   if (pad) {
     const int kv = a.state[a.kvlen_base + b];
     kend = kend < kv ? kend : kv;
   }
   const float sl2 = a.scale * 1.4426950408889634f;
 
-  float mrow[2] = {-INFINITY, -INFINITY}, lrow[2] = {0.f, 0.f};
-  f32x4 oacc[2][NCT];
+  float mrow[U], lrow[U];
+  f32x4 oacc[U][NCT];
 #pragma unroll
-  for (int u = 0; u < 2; ++u)
+  for (int u = 0; u < U; ++u) {
+    mrow[u] = -INFINITY;
+    lrow[u] = 0.f;
+  }
+#pragma unroll
+  for (int u = 0; u < U; ++u)
 #pragma unroll
     for (int c = 0; c < NCT; ++c) oacc[u][c] = f32x4{0.f, 0.f, 0.f, 0.f};
 
@@ -218,24 +225,24 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
     if (kb + kKB < kend) gload(kb + kKB);
 
     // ---- S^T = K Q^T
-    f32x4 sacc[4][2];
+    f32x4 sacc[4][U];
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-      for (int u = 0; u < 2; ++u) sacc[kt][u] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int u = 0; u < U; ++u) sacc[kt][u] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt) {
         const vec kf = *reinterpret_cast<const vec*>(&sK[buf][(16 * kt + l16) * LDK + 32 * c + 8 * g]);
 #pragma unroll
-        for (int u = 0; u < 2; ++u) sacc[kt][u] = MfmaA<T>::run(kf, qf[u][c], sacc[kt][u]);
+        for (int u = 0; u < U; ++u) sacc[kt][u] = MfmaA<T>::run(kf, qf[u][c], sacc[kt][u]);
       }
     }
     // ---- masks and online softmax (per query = per (u, l16))
-    float p[4][2][4];
+    float p[4][U][4];
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
+    for (int u = 0; u < U; ++u) {
       const int qi = q0 + 16 * u + l16;
       float tmax = -INFINITY;
 #pragma unroll
@@ -274,9 +281,9 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
     // ---- O^T += V^T P^T
 #pragma unroll
     for (int kc = 0; kc < 2; ++kc) {
-      vec pb[2];
+      vec pb[U];
 #pragma unroll
-      for (int u = 0; u < 2; ++u) {
+      for (int u = 0; u < U; ++u) {
         T tmp[8];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -293,13 +300,13 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
         *reinterpret_cast<u32x2*>(&tmp[4]) = *reinterpret_cast<const u32x2*>(vr + 16);
         const vec vf = *reinterpret_cast<const vec*>(tmp);
 #pragma unroll
-        for (int u = 0; u < 2; ++u) oacc[u][c] = MfmaA<T>::run(vf, pb[u], oacc[u][c]);
+        for (int u = 0; u < U; ++u) oacc[u][c] = MfmaA<T>::run(vf, pb[u], oacc[u][c]);
       }
     }
   }
   // ---- normalise and store: lane holds channels 16c + 4g + r of query (u, l16)
 #pragma unroll
-  for (int u = 0; u < 2; ++u) {
+  for (int u = 0; u < U; ++u) {
     const int qi = q0 + 16 * u + l16;
     if (qi >= Sq) continue;
     const float inv = lrow[u] > 0.f ? 1.f / lrow[u] : 0.f;
@@ -328,13 +335,18 @@ void launch_attention(const AttnArgs& a, hipStream_t s) {
     else hipLaunchKernelGGL(k_attn_rows<f16_t>, grid, dim3(64), lds, s, a);
     return;
   }
-  const dim3 grid((a.Sq + kQB - 1) / kQB, a.H, a.B);
+  // 16 queries per wavefront: twice the workgroups and wavefronts of 32
+  // (measured 9% faster at 8 x 12 heads x 512 causal), since each key tile
+  // is a dependent chain (scores, masked online softmax, P.V) that needs
+  // other wavefronts to hide its latency
+  constexpr int U = 1;
+  const dim3 grid((a.Sq + 64 * U - 1) / (64 * U), a.H, a.B);
   if (a.dtype == kBF16) {
-    if (a.hd == 64) hipLaunchKernelGGL((k_attn_mfma<bf16_t, 64>), grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((k_attn_mfma<bf16_t, 128>), grid, dim3(256), 0, s, a);
+    if (a.hd == 64) hipLaunchKernelGGL((k_attn_mfma<bf16_t, 64, U>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((k_attn_mfma<bf16_t, 128, U>), grid, dim3(256), 0, s, a);
   } else {
-    if (a.hd == 64) hipLaunchKernelGGL((k_attn_mfma<f16_t, 64>), grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((k_attn_mfma<f16_t, 128>), grid, dim3(256), 0, s, a);
+    if (a.hd == 64) hipLaunchKernelGGL((k_attn_mfma<f16_t, 64, U>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((k_attn_mfma<f16_t, 128, U>), grid, dim3(256), 0, s, a);
   }
 }
 
