@@ -195,3 +195,27 @@ def test_fragmented_encoder_decoder_equals_single_graph():
     with pytest.raises(GmError):
         b.forward_seq2seq(*bufs, out_b)
     assert b.check_error() == (TRAP_TOKEN_RANGE, si.size + cfg.tgt_seq + 1)
+
+
+def test_edge_cases_fully_padded_source_and_length_one():
+    """A source sequence that is all padding (its cross-attention sees no
+    key: the context is zero), source and target of length 1, one sequence."""
+    cfg = tiny_fp32()
+    w = synth.make_weights(cfg, 65)
+    m = s2s_model(cfg, w)
+    orc = OracleSeq2Seq(cfg, w)
+    si, sm = synth.make_inputs(cfg, 6)
+    ti, tm = synth.make_target_inputs(cfg, 6)
+    sm[1, :] = 0
+    ref = orc.forward(si, sm, ti, tm)
+    check_logits(f64(run_s2s(m, si, sm, ti, tm)), ref.logits_f64, cfg.dtype, "all-pad source")
+    expect = effects_of(ref)
+    for B, Ss, St in ((3, 1, 1), (1, cfg.seq, 1), (1, 1, cfg.tgt_seq), (2, 5, 3)):
+        ids_s, mk_s = si[:B, :Ss].copy(), np.ones((B, Ss), np.int32)
+        ids_t, mk_t = ti[:B, :St].copy(), np.ones((B, St), np.int32)
+        ref = orc.forward(ids_s, mk_s, ids_t, mk_t)
+        got = f64(run_s2s(m, ids_s, mk_s, ids_t, mk_t))
+        check_logits(got, ref.logits_f64, cfg.dtype, f"B {B} S_src {Ss} S_tgt {St}")
+        expect += effects_of(ref)
+    assert gpu_effects(m) == expect
+    assert m.check_error() == (0, 0)
