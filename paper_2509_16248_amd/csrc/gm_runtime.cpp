@@ -90,6 +90,13 @@ struct gm_model {
   float *rope_cos = nullptr, *rope_sin = nullptr;
   void* fifo = nullptr;
   hipStream_t cap_stream = nullptr;
+  // further batch-part branches of a forward: their streams and the
+  // fork/join events (the branches are independent, so the GPU overlaps one
+  // part's latency-bound kernels with another part's GEMMs)
+  static constexpr int kMaxParts = 4;
+  hipStream_t aux_stream[kMaxParts - 1] = {};
+  hipEvent_t ev_fork = nullptr, ev_join[kMaxParts - 1] = {};
+  int split_parts = 2;
   std::vector<GraphEntry> graphs;
   gm_stats stats;
   int exec_mode = GM_EXEC_GRAPH;
@@ -378,8 +385,20 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
   P(GM_K_EMBED, -1, 0.0, static_cast<double>(T) * d * es * (c.pos == GM_POS_LEARNED ? 3 : 2));
   r.ids = nullptr;
 
+  // The layers and the head over sequences [b0, b0 + nb) on stream s.
+  auto layers_and_head = [&](hipStream_t s, int b0, int nb) {
+  const int T = nb * S;
+  const size_t ro = static_cast<size_t>(b0) * S;   // first row of this part
+  char* hh = static_cast<char*>(m->h) + ro * d * m->esz;
+  char* aa = static_cast<char*>(m->a) + ro * d * m->esz;
+  char* qq = static_cast<char*>(m->qkv) + ro * 3 * d * m->esz;
+  char* cc = static_cast<char*>(m->ctx) + ro * d * m->esz;
+  char* ffb = static_cast<char*>(m->f) + ro * ff * m->esz;
+  char* tt = m->tmp ? static_cast<char*>(m->tmp) + ro * d * m->esz : nullptr;
+  char* lg = static_cast<char*>(logits) + ro * c.vocab * m->esz;
   auto norm_rows = [&](void* x, void* out, const void* g, const void* b, int site) {
     RowArgs q = r;
+    q.rows = T;
     q.x = x;
     q.out = out;
     q.norm = normk;
@@ -437,21 +456,21 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
 
   AttnArgs at{};
   at.dtype = m->dtype;
-  at.B = B;
+  at.B = nb;
   at.Sq = at.Sk = S;
   at.H = c.n_heads;
   at.hd = hd;
   at.d = d;
-  at.q = m->qkv;
+  at.q = qq;
   at.ldq = 3 * d;
-  at.k = static_cast<const char*>(m->qkv) + d * m->esz;
-  at.v = static_cast<const char*>(m->qkv) + 2 * d * m->esz;
+  at.k = static_cast<const char*>(qq) + d * m->esz;
+  at.v = static_cast<const char*>(qq) + 2 * d * m->esz;
   at.ldkv = 3 * d;
-  at.ctx = m->ctx;
-  at.mask = mask;
+  at.ctx = cc;
+  at.mask = mask ? mask + static_cast<size_t>(b0) * S : nullptr;
   at.state = m->state;
   at.pad_slot = kPadAny;
-  at.kvlen_base = kKvLenBase;
+  at.kvlen_base = kKvLenBase + b0;
   at.causal = c.causal;
   at.scale = 1.0f / sqrtf(static_cast<float>(hd));
 
@@ -460,7 +479,7 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
   const int up_n = c.ffn == GM_FFN_GELU ? ff : 2 * ff;
   const int qkv_epi = c.pos == GM_POS_ROTARY ? kEpiRope : kEpiStore;
   const double pairs = c.causal ? 0.5 * S * (S + 1.0) : static_cast<double>(S) * S;
-  const double attn_flops = 4.0 * hd * pairs * B * c.n_heads;
+  const double attn_flops = 4.0 * hd * pairs * nb * c.n_heads;
   const double attn_bytes = es * (static_cast<double>(T) * 3 * d + static_cast<double>(T) * d);
   KvArgs kv{};
   kv.dtype = m->dtype;
@@ -469,7 +488,7 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
   kv.pos = m->dpos;
   kv.mask = mask;
   kv.state = m->state;
-  kv.qkv = m->qkv;
+  kv.qkv = qq;
   kv.d = d;
   kv.H = c.n_heads;
   kv.hd = hd;
@@ -481,11 +500,11 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
   da.H = c.n_heads;
   da.hd = hd;
   da.d = d;
-  da.qkv = m->qkv;
+  da.qkv = qq;
   da.valid = m->kv_valid;
   da.max_seq = c.max_seq;
   da.pos = m->dpos;
-  da.ctx = m->ctx;
+  da.ctx = cc;
   da.part = m->dpart;
   {
     // split the keys only when there are fewer than ~100 (sequence, head)
@@ -524,43 +543,67 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
     const LayerBufs& L = m->layers[l];
     const int s0 = ns ? 2 * l : -1, s1 = ns ? 2 * l + 1 : -1;
     if (pre) {
-      norm_rows(m->h, m->a, L.ln1_g, L.ln1_b, prev_site);
-      gemm(GM_K_GEMM_QKV, m->a, d, L.wqkv, 3 * d, qkv_epi, L.bqkv, m->qkv, 3 * d, nullptr, -1);
+      norm_rows(hh, aa, L.ln1_g, L.ln1_b, prev_site);
+      gemm(GM_K_GEMM_QKV, aa, d, L.wqkv, 3 * d, qkv_epi, L.bqkv, qq, 3 * d, nullptr, -1);
       attention();
-      gemm(GM_K_GEMM_O, m->ctx, d, L.wo, d, kEpiResid, L.bo, m->h, d, m->h, s0);
-      norm_rows(m->h, m->a, L.ln2_g, L.ln2_b, s0);
-      gemm(GM_K_GEMM_UP, m->a, d, L.w1, up_n, up_epi, L.b1, m->f, ff, nullptr, -1);
-      gemm(GM_K_GEMM_DOWN, m->f, ff, L.w2, d, kEpiResid, L.b2, m->h, d, m->h, s1);
+      gemm(GM_K_GEMM_O, cc, d, L.wo, d, kEpiResid, L.bo, hh, d, hh, s0);
+      norm_rows(hh, aa, L.ln2_g, L.ln2_b, s0);
+      gemm(GM_K_GEMM_UP, aa, d, L.w1, up_n, up_epi, L.b1, ffb, ff, nullptr, -1);
+      gemm(GM_K_GEMM_DOWN, ffb, ff, L.w2, d, kEpiResid, L.b2, hh, d, hh, s1);
       prev_site = s1;
     } else {
-      gemm(GM_K_GEMM_QKV, m->h, d, L.wqkv, 3 * d, qkv_epi, L.bqkv, m->qkv, 3 * d, nullptr, -1);
+      gemm(GM_K_GEMM_QKV, hh, d, L.wqkv, 3 * d, qkv_epi, L.bqkv, qq, 3 * d, nullptr, -1);
       attention();
-      gemm(GM_K_GEMM_O, m->ctx, d, L.wo, d, kEpiResid, L.bo, m->tmp, d, m->h, -1);
-      norm_rows(m->tmp, m->h, L.ln1_g, L.ln1_b, -1);
-      gemm(GM_K_GEMM_UP, m->h, d, L.w1, up_n, up_epi, L.b1, m->f, ff, nullptr, -1);
-      gemm(GM_K_GEMM_DOWN, m->f, ff, L.w2, d, kEpiResid, L.b2, m->tmp, d, m->h, -1);
-      norm_rows(m->tmp, m->h, L.ln2_g, L.ln2_b, -1);
+      gemm(GM_K_GEMM_O, cc, d, L.wo, d, kEpiResid, L.bo, tt, d, hh, -1);
+      norm_rows(tt, hh, L.ln1_g, L.ln1_b, -1);
+      gemm(GM_K_GEMM_UP, hh, d, L.w1, up_n, up_epi, L.b1, ffb, ff, nullptr, -1);
+      gemm(GM_K_GEMM_DOWN, ffb, ff, L.w2, d, kEpiResid, L.b2, tt, d, hh, -1);
+      norm_rows(tt, hh, L.ln2_g, L.ln2_b, -1);
     }
     if (c.log_hidden) {
       // `logger.info(..., h.abs().amax(per sequence))`: a tensor-valued log,
       // its value taken here and replayed after the forward
       if (on())
-        launch_log_seqmax(m->h, m->dtype, B, S, d, m->log_stage, l, m->state,
+        launch_log_seqmax(hh, m->dtype, B, S, d, m->log_stage, l, m->state,
                           pre && ns ? 2 * l + 1 : -1, thr, s);
       P(GM_K_LOG, l, 0.0, es * T * d);
       brk(kCutLog + l);   // original program: the value is copied to the host to print it
     }
   }
   cur_layer = -1;
-  const void* z = m->h;
+  const void* z = hh;
   if (pre) {
-    norm_rows(m->h, m->a, m->lnf_g, m->lnf_b, prev_site);
-    z = m->a;
+    norm_rows(hh, aa, m->lnf_g, m->lnf_b, prev_site);
+    z = aa;
   }
-  gemm(GM_K_GEMM_HEAD, z, d, m->head, c.vocab, kEpiStore, nullptr, logits, c.vocab, nullptr, -1);
+  gemm(GM_K_GEMM_HEAD, z, d, m->head, c.vocab, kEpiStore, nullptr, lg, c.vocab, nullptr, -1);
   if (dec && dec->next) {
-    launch_argmax(logits, m->dtype, B, c.vocab, dec->next, s);
+    launch_argmax(lg, m->dtype, B, c.vocab, dec->next, s);
     P(GM_K_ARGMAX, -1, 0.0, es * B * static_cast<double>(c.vocab));
+  }
+  };
+  // Independent batch-part branches (fork/join on auxiliary streams) where
+  // nothing couples the sequences inside the layers: no clamp (its decision
+  // is batch-global), no tensor log, no KV cache, not a decode step, profile
+  // or graph-broken run, and every part large enough for the tiled GEMMs,
+  // whose per-element arithmetic does not depend on M, so the results are
+  // the same bits as one branch.
+  int parts = m->split_parts < B ? m->split_parts : B;
+  while (parts > 1 && (B / parts) * S <= 16) --parts;
+  if (dec || prof || seg || c.fp16_clamp || c.log_hidden || c.kv_cache) parts = 1;
+  if (parts > 1) {
+    (void)hipEventRecord(m->ev_fork, s);
+    for (int i = 0; i + 1 < parts; ++i) (void)hipStreamWaitEvent(m->aux_stream[i], m->ev_fork, 0);
+    for (int i = 0; i < parts; ++i) {
+      const int b0 = B * i / parts, b1 = B * (i + 1) / parts;
+      layers_and_head(i == 0 ? s : m->aux_stream[i - 1], b0, b1 - b0);
+    }
+    for (int i = 0; i + 1 < parts; ++i) {
+      (void)hipEventRecord(m->ev_join[i], m->aux_stream[i]);
+      (void)hipStreamWaitEvent(s, m->ev_join[i], 0);
+    }
+  } else {
+    layers_and_head(s, 0, B);
   }
   if (c.kv_cache && on()) launch_seqlen_update(m->seqlen, m->dpos, m->state, B, dec ? 1 : 0, s);
   if (on())
@@ -824,6 +867,11 @@ void gm_model_destroy(gm_model* m) {
   for (auto& f : m->frags)
     for (hipGraphExec_t e : f.execs) hipGraphExecDestroy(e);
   if (m->cap_stream) hipStreamDestroy(m->cap_stream);
+  for (int i = 0; i < gm_model::kMaxParts - 1; ++i) {
+    if (m->aux_stream[i]) hipStreamDestroy(m->aux_stream[i]);
+    if (m->ev_join[i]) hipEventDestroy(m->ev_join[i]);
+  }
+  if (m->ev_fork) hipEventDestroy(m->ev_fork);
   for (void* p : m->allocs) hipFree(p);
   delete m;
 }
@@ -1091,7 +1139,17 @@ int gm_model_create(const gm_config* cfg, const gm_weights* w, gm_model** out) {
     if (e != hipSuccess) return fail(hip_fail(e, "rope init"));
   }
   e = hipStreamCreateWithFlags(&m->cap_stream, hipStreamNonBlocking);
+  for (int i = 0; e == hipSuccess && i < gm_model::kMaxParts - 1; ++i)
+    e = hipStreamCreateWithFlags(&m->aux_stream[i], hipStreamNonBlocking);
   if (e != hipSuccess) return fail(hip_fail(e, "hipStreamCreate"));
+  e = hipEventCreateWithFlags(&m->ev_fork, hipEventDisableTiming);
+  for (int i = 0; e == hipSuccess && i < gm_model::kMaxParts - 1; ++i)
+    e = hipEventCreateWithFlags(&m->ev_join[i], hipEventDisableTiming);
+  if (e != hipSuccess) return fail(hip_fail(e, "hipEventCreate"));
+  if (const char* v = getenv("GM_SPLIT_PARTS")) {
+    const int n = atoi(v);
+    m->split_parts = n < 1 ? 1 : (n > gm_model::kMaxParts ? gm_model::kMaxParts : n);
+  }
   e = hipDeviceSynchronize();
   if (e != hipSuccess) return fail(hip_fail(e, "create"));
   *out = m;

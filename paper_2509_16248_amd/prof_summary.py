@@ -4,6 +4,10 @@ reports as ``roofline.traffic``.
 
     python -m paper_2509_16248_amd.prof_summary FETCH_DIR WRITE_DIR OUT.json
 
+Only the launches of the whole-batch shapes are counted: bench.py's
+roofline is measured on its eager per-kernel profile, which runs the whole
+batch per launch (the graph splits the batch into concurrent parts).
+
 Calibration: both runs contain the runtime's copy kernel moving the token
 embedding (vocab x d_model x 2 bytes) into library memory; the largest such
 dispatch gives the bytes each counter unit stands for (FETCH_SIZE of a copy
@@ -51,9 +55,12 @@ def summarize(fetch_dir, write_dir, src):
     tot_f = tot_w = n = 0
     for rows, key in ((f, "fetch"), (w, "write")):
         for k, g, v in rows:
-            if not k.startswith(KERNEL):
+            # the whole-batch launches (the eager per-kernel profile that
+            # bench.py's roofline is measured on); the graph's batch-part
+            # launches have other grids
+            if not k.startswith(KERNEL) or g not in SHAPES:
                 continue
-            name = SHAPES.get(g, f"grid {g}")
+            name = SHAPES[g]
             e = per.setdefault(name, {"dispatches": 0, "fetch_kib": [], "write_kib": []})
             e[key + "_kib"].append(v)
     for name, e in per.items():
