@@ -643,6 +643,40 @@ void enqueue_seq2seq(gm_model* m, int B, int Ss, const int32_t* src_ids, const i
   P(GM_K_PROLOGUE, -1, 0.0, 8.0 * Ts);
   brk(kCutGuards);   // original program: the source's guards and mask.any() read on the host
 
+  // The target's guards and padding predicate: before the decoder (after the
+  // encoder) in one branch, where the graph-broken program reads them; before
+  // the fork when the batch runs as parts.
+  auto target_prologue = [&](hipStream_t s) {
+    if (on())
+      launch_prologue(tgt_ids, tgt_mask, B, St, c.vocab, 0, 0, 0, nullptr, 0, nullptr, 0, 0,
+                      m->state, s, 1, Ts, kKvLenBase + c.max_batch);
+    P(GM_K_PROLOGUE, -1, 0.0, 8.0 * Tt);
+    brk(kCutGuardsTgt);   // original program: the target's guards and mask.any() read on the host
+  };
+  // Sequences [b0, b0 + nb) on stream s: part p's encoder and decoder rows
+  // start at row b0 * S_src of every activation buffer (the decoder rows fit
+  // in the part's encoder rows since S_tgt <= S_src when the batch is split).
+  // Batch parts run as concurrent graph branches when nothing couples them
+  // (not profiled or graph-broken, parts above 16 rows).
+  const int b_half = B / 2;
+  const bool split = m->split_parts > 1 && !prof && !seg && St <= Ss && b_half >= 1 &&
+                     b_half * St > 16;
+  auto part = [&](hipStream_t s, int b0, int nb) {
+  const int Tsp = nb * Ss, Ttp = nb * St;
+  const size_t ro = static_cast<size_t>(b0) * Ss, rt = static_cast<size_t>(b0) * St;
+  char* hh = static_cast<char*>(m->h) + ro * d * m->esz;
+  char* aa = static_cast<char*>(m->a) + ro * d * m->esz;
+  char* qq = static_cast<char*>(m->qkv) + ro * 3 * d * m->esz;
+  char* cc = static_cast<char*>(m->ctx) + ro * d * m->esz;
+  char* ffb = static_cast<char*>(m->f) + ro * ff * m->esz;
+  char* mm = static_cast<char*>(m->mem) + ro * d * m->esz;
+  char* kk = static_cast<char*>(m->kvc) + ro * nd * 2 * d * m->esz;
+  char* qcc = static_cast<char*>(m->qc) + rt * d * m->esz;
+  char* lg = static_cast<char*>(logits) + rt * c.vocab * m->esz;
+  const int32_t* sids = src_ids + ro;
+  const int32_t* tids = tgt_ids + rt;
+  const int32_t* smask = src_mask + ro;
+  const int32_t* tmask = tgt_mask + rt;
   RowArgs r{};
   r.dtype = m->dtype;
   r.d = d;
@@ -657,8 +691,8 @@ void enqueue_seq2seq(gm_model* m, int B, int Ss, const int32_t* src_ids, const i
     e.ids = ids;
     e.pos_emb = pos;
     e.seq = S;
-    e.x = m->h;
-    e.out = m->h;
+    e.x = hh;
+    e.out = hh;
     e.norm = -1;
     if (on()) launch_rownorm(e, s);
     P(GM_K_EMBED, -1, 0.0, static_cast<double>(rows) * d * es * 3);
@@ -704,11 +738,11 @@ void enqueue_seq2seq(gm_model* m, int B, int Ss, const int32_t* src_ids, const i
   };
   AttnArgs at{};
   at.dtype = m->dtype;
-  at.B = B;
+  at.B = nb;
   at.H = c.n_heads;
   at.hd = hd;
   at.d = d;
-  at.ctx = m->ctx;
+  at.ctx = cc;
   at.state = m->state;
   at.scale = 1.0f / sqrtf(static_cast<float>(hd));
   auto attention = [&](int kind, int Sq, int Sk, const void* q, int ldq, const void* k, int ldkv,
@@ -727,65 +761,73 @@ void enqueue_seq2seq(gm_model* m, int B, int Ss, const int32_t* src_ids, const i
     a.causal = causal;
     if (on()) launch_attention(a, s);
     const double pairs = causal ? 0.5 * Sq * (Sq + 1.0) : static_cast<double>(Sq) * Sk;
-    P(kind, cur_layer, 4.0 * hd * pairs * B * c.n_heads,
-      es * (static_cast<double>(B) * Sq * 2 * d + static_cast<double>(B) * Sk * 2 * d));
+    P(kind, cur_layer, 4.0 * hd * pairs * nb * c.n_heads,
+      es * (static_cast<double>(nb) * Sq * 2 * d + static_cast<double>(nb) * Sk * 2 * d));
   };
   const int up_epi = c.ffn == GM_FFN_GELU ? kEpiGelu
                      : c.ffn == GM_FFN_GEGLU ? kEpiGatedGelu : kEpiGatedSilu;
   const int up_n = c.ffn == GM_FFN_GELU ? ff : 2 * ff;
-  char* qkv = static_cast<char*>(m->qkv);
+  char* qkv = static_cast<char*>(qq);
   auto block_ffn = [&](int rows, const LayerBufs& L) {
-    norm_rows(rows, m->h, m->a, L.ln2_g, L.ln2_b);
-    gemm(GM_K_GEMM_UP, rows, m->a, d, L.w1, up_n, up_epi, L.b1, m->f, ff, nullptr);
-    gemm(GM_K_GEMM_DOWN, rows, m->f, ff, L.w2, d, kEpiResid, L.b2, m->h, d, m->h);
+    norm_rows(rows, hh, aa, L.ln2_g, L.ln2_b);
+    gemm(GM_K_GEMM_UP, rows, aa, d, L.w1, up_n, up_epi, L.b1, ffb, ff, nullptr);
+    gemm(GM_K_GEMM_DOWN, rows, ffb, ff, L.w2, d, kEpiResid, L.b2, hh, d, hh);
   };
 
   // encoder (bidirectional; the source's padding branch)
-  embed(Ts, Ss, src_ids, m->enc_pos_emb);
+  embed(Tsp, Ss, sids, m->enc_pos_emb);
   for (int l = 0; l < c.n_layers; ++l) {
     cur_layer = l;
     const LayerBufs& L = m->layers[l];
-    norm_rows(Ts, m->h, m->a, L.ln1_g, L.ln1_b);
-    gemm(GM_K_GEMM_QKV, Ts, m->a, d, L.wqkv, 3 * d, kEpiStore, L.bqkv, m->qkv, 3 * d, nullptr);
-    attention(GM_K_ATTENTION, Ss, Ss, qkv, 3 * d, qkv + d * m->esz, 3 * d, src_mask, kPadAny,
-              kKvLenBase, 0);
-    gemm(GM_K_GEMM_O, Ts, m->ctx, d, L.wo, d, kEpiResid, L.bo, m->h, d, m->h);
-    block_ffn(Ts, L);
+    norm_rows(Tsp, hh, aa, L.ln1_g, L.ln1_b);
+    gemm(GM_K_GEMM_QKV, Tsp, aa, d, L.wqkv, 3 * d, kEpiStore, L.bqkv, qq, 3 * d, nullptr);
+    attention(GM_K_ATTENTION, Ss, Ss, qkv, 3 * d, qkv + d * m->esz, 3 * d, smask, kPadAny,
+              kKvLenBase + b0, 0);
+    gemm(GM_K_GEMM_O, Tsp, cc, d, L.wo, d, kEpiResid, L.bo, hh, d, hh);
+    block_ffn(Tsp, L);
   }
   cur_layer = -1;
-  norm_rows(Ts, m->h, m->mem, m->enc_lnf_g, m->enc_lnf_b);
+  norm_rows(Tsp, hh, mm, m->enc_lnf_g, m->enc_lnf_b);
   // k | v of every decoder layer from the encoder output, one GEMM
-  gemm(GM_K_GEMM_XKV, Ts, m->mem, d, m->wkv_all, nd * 2 * d, kEpiStore, m->bkv_all, m->kvc,
+  gemm(GM_K_GEMM_XKV, Tsp, mm, d, m->wkv_all, nd * 2 * d, kEpiStore, m->bkv_all, kk,
        nd * 2 * d, nullptr);
 
   // decoder (causal self-attention under the target's padding branch,
   // cross-attention under the source's); its inputs' guards merge into the
   // forward's trap word
-  if (on())
-    launch_prologue(tgt_ids, tgt_mask, B, St, c.vocab, 0, 0, 0, nullptr, 0, nullptr, 0, 0,
-                    m->state, s, 1, Ts, kKvLenBase + c.max_batch);
-  P(GM_K_PROLOGUE, -1, 0.0, 8.0 * Tt);
-  brk(kCutGuardsTgt);   // original program: the target's guards and mask.any() read on the host
-  embed(Tt, St, tgt_ids, m->pos_emb);
+  if (!split) target_prologue(s);
+  embed(Ttp, St, tids, m->pos_emb);
   for (int l = 0; l < nd; ++l) {
     cur_layer = c.n_layers + l;
     const LayerBufs& L = m->dec_layers[l];
     const CrossBufs& X = m->dec_cross[l];
-    norm_rows(Tt, m->h, m->a, L.ln1_g, L.ln1_b);
-    gemm(GM_K_GEMM_QKV, Tt, m->a, d, L.wqkv, 3 * d, kEpiStore, L.bqkv, m->qkv, 3 * d, nullptr);
-    attention(GM_K_ATTENTION, St, St, qkv, 3 * d, qkv + d * m->esz, 3 * d, tgt_mask, kPadAnyTgt,
-              kKvLenBase + c.max_batch, 1);
-    gemm(GM_K_GEMM_O, Tt, m->ctx, d, L.wo, d, kEpiResid, L.bo, m->h, d, m->h);
-    norm_rows(Tt, m->h, m->a, X.lnc_g, X.lnc_b);
-    gemm(GM_K_GEMM_XQ, Tt, m->a, d, X.wq, d, kEpiStore, X.bq, m->qc, d, nullptr);
-    attention(GM_K_XATTN, St, Ss, m->qc, d, static_cast<char*>(m->kvc) + static_cast<size_t>(l) * 2 * d * m->esz,
-              nd * 2 * d, src_mask, kPadAny, kKvLenBase, 0);
-    gemm(GM_K_GEMM_XO, Tt, m->ctx, d, X.wo, d, kEpiResid, X.bo, m->h, d, m->h);
-    block_ffn(Tt, L);
+    norm_rows(Ttp, hh, aa, L.ln1_g, L.ln1_b);
+    gemm(GM_K_GEMM_QKV, Ttp, aa, d, L.wqkv, 3 * d, kEpiStore, L.bqkv, qq, 3 * d, nullptr);
+    attention(GM_K_ATTENTION, St, St, qkv, 3 * d, qkv + d * m->esz, 3 * d, tmask, kPadAnyTgt,
+              kKvLenBase + c.max_batch + b0, 1);
+    gemm(GM_K_GEMM_O, Ttp, cc, d, L.wo, d, kEpiResid, L.bo, hh, d, hh);
+    norm_rows(Ttp, hh, aa, X.lnc_g, X.lnc_b);
+    gemm(GM_K_GEMM_XQ, Ttp, aa, d, X.wq, d, kEpiStore, X.bq, qcc, d, nullptr);
+    attention(GM_K_XATTN, St, Ss, qcc, d, static_cast<char*>(kk) + static_cast<size_t>(l) * 2 * d * m->esz,
+              nd * 2 * d, smask, kPadAny, kKvLenBase + b0, 0);
+    gemm(GM_K_GEMM_XO, Ttp, cc, d, X.wo, d, kEpiResid, X.bo, hh, d, hh);
+    block_ffn(Ttp, L);
   }
   cur_layer = -1;
-  norm_rows(Tt, m->h, m->a, m->lnf_g, m->lnf_b);
-  gemm(GM_K_GEMM_HEAD, Tt, m->a, d, m->head, c.vocab, kEpiStore, nullptr, logits, c.vocab, nullptr);
+  norm_rows(Ttp, hh, aa, m->lnf_g, m->lnf_b);
+  gemm(GM_K_GEMM_HEAD, Ttp, aa, d, m->head, c.vocab, kEpiStore, nullptr, lg, c.vocab, nullptr);
+  };
+  if (split) {
+    target_prologue(s);
+    (void)hipEventRecord(m->ev_fork, s);
+    (void)hipStreamWaitEvent(m->aux_stream[0], m->ev_fork, 0);
+    part(s, 0, b_half);
+    part(m->aux_stream[0], b_half, B - b_half);
+    (void)hipEventRecord(m->ev_join[0], m->aux_stream[0]);
+    (void)hipStreamWaitEvent(s, m->ev_join[0], 0);
+  } else {
+    part(s, 0, B);
+  }
   if (on()) launch_emit_effects(m->state, m->fifo, kFifoCap, 0, nullptr, nullptr, 0, 0, B, 1, s);
   P(GM_K_EFFECTS, -1, 0.0, 0.0);
 }
