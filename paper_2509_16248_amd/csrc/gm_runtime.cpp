@@ -584,24 +584,30 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
   };
   // Independent batch-part branches (fork/join on auxiliary streams) where
   // nothing couples the sequences inside the layers: no clamp (its decision
-  // is batch-global), no tensor log, no KV cache, not a decode step, profile
-  // or graph-broken run, and every part large enough for the tiled GEMMs,
+  // is batch-global), no tensor log, no KV cache, not a decode step or
+  // profile, and every part large enough for the tiled GEMMs,
   // whose per-element arithmetic does not depend on M, so the results are
   // the same bits as one branch.
   int parts = m->split_parts < B ? m->split_parts : B;
   while (parts > 1 && (B / parts) * S <= 16) --parts;
-  if (dec || prof || seg || c.fp16_clamp || c.log_hidden || c.kv_cache) parts = 1;
+  if (dec || prof || c.fp16_clamp || c.log_hidden || c.kv_cache) parts = 1;
   if (parts > 1) {
-    (void)hipEventRecord(m->ev_fork, s);
-    for (int i = 0; i + 1 < parts; ++i) (void)hipStreamWaitEvent(m->aux_stream[i], m->ev_fork, 0);
+    // (the graph-broken run splits the same way: its only cut, the guards,
+    // lies before the fork, and the fork and join go into the segment that
+    // holds the layers)
+    if (on()) {
+      (void)hipEventRecord(m->ev_fork, s);
+      for (int i = 0; i + 1 < parts; ++i) (void)hipStreamWaitEvent(m->aux_stream[i], m->ev_fork, 0);
+    }
     for (int i = 0; i < parts; ++i) {
       const int b0 = B * i / parts, b1 = B * (i + 1) / parts;
       layers_and_head(i == 0 ? s : m->aux_stream[i - 1], b0, b1 - b0);
     }
-    for (int i = 0; i + 1 < parts; ++i) {
-      (void)hipEventRecord(m->ev_join[i], m->aux_stream[i]);
-      (void)hipStreamWaitEvent(s, m->ev_join[i], 0);
-    }
+    if (on())
+      for (int i = 0; i + 1 < parts; ++i) {
+        (void)hipEventRecord(m->ev_join[i], m->aux_stream[i]);
+        (void)hipStreamWaitEvent(s, m->ev_join[i], 0);
+      }
   } else {
     layers_and_head(s, 0, B);
   }
