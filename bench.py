@@ -147,7 +147,7 @@ def seq2seq_bench(args):
                 "host_syncs_per_forward": (s1["host_syncs_in_forward"] - s0["host_syncs_in_forward"]) / args.steps}
 
     g = timed("graph")
-    f = timed("fragmented")
+    f = None if args.no_fragmented else timed("fragmented")
     code = m.check_error()
     kernels = m.stats()["kernels_per_forward"]
     m.close()
@@ -158,7 +158,7 @@ def seq2seq_bench(args):
             "tokens_per_forward": tokens, "kernels_per_forward": kernels,
             "tokens_per_s": round(tokens / (g["ms_per_step"] * 1e-3), 1),
             "single_graph": g, "fragmented": f,
-            "steady_speedup": round(f["wall_ms_per_step"] / g["wall_ms_per_step"], 3),
+            "steady_speedup": round(f["wall_ms_per_step"] / g["wall_ms_per_step"], 3) if f else None,
             "trap": list(code)}
 
 
