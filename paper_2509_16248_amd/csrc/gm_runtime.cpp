@@ -415,7 +415,7 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
   ga.state = m->state;
   ga.site = -1;
   ga.seq = S;
-  ga.pos = dec ? m->dpos : nullptr;
+  ga.pos = dec ? m->dpos + b0 : nullptr;
   ga.head_dim = hd;
   ga.d_model = d;
   ga.rope_cos = m->rope_cos;
@@ -427,9 +427,11 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
     GemmArgs q = ga;
     if (dec && kind == GM_K_GEMM_QKV) {
       // a decode step stores this layer's new k and v from the epilogue
-      q.kc = m->kc[cur_layer];
-      q.vc = m->vc[cur_layer];
-      q.kv_valid = m->kv_valid;
+      // this part's sequences in the cache ([B][H][max_seq][hd])
+      const size_t co = static_cast<size_t>(b0) * c.n_heads * c.max_seq * hd * m->esz;
+      q.kc = static_cast<char*>(m->kc[cur_layer]) + co;
+      q.vc = static_cast<char*>(m->vc[cur_layer]) + co;
+      q.kv_valid = m->kv_valid + static_cast<size_t>(b0) * c.max_seq;
       q.kv_max_seq = c.max_seq;
       q.heads = c.n_heads;
     }
@@ -496,14 +498,14 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
   kv.max_seq = c.max_seq;
   DecAttnArgs da{};
   da.dtype = m->dtype;
-  da.B = B;
+  da.B = nb;
   da.H = c.n_heads;
   da.hd = hd;
   da.d = d;
   da.qkv = qq;
-  da.valid = m->kv_valid;
+  da.valid = m->kv_valid + static_cast<size_t>(b0) * c.max_seq;
   da.max_seq = c.max_seq;
-  da.pos = m->dpos;
+  da.pos = m->dpos + b0;
   da.ctx = cc;
   da.part = m->dpart;
   {
@@ -516,6 +518,8 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
     da.chunk = 64 * ((c.max_seq + 64 * want - 1) / (64 * want));
     da.nsplit = (c.max_seq + da.chunk - 1) / da.chunk;
   }
+  // this part's rows of the split-key workspace ([B][H][nsplit][hd + 2])
+  if (m->dpart) da.part = m->dpart + static_cast<size_t>(b0) * c.n_heads * da.nsplit * (hd + 2);
   da.scale = at.scale;
   auto attention = [&]() {
     if (c.kv_cache && !dec) {
@@ -527,8 +531,9 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
       P(GM_K_KV_STORE, cur_layer, 0.0, 4.0 * T * d * es);
     }
     if (dec) {
-      da.kc = m->kc[cur_layer];
-      da.vc = m->vc[cur_layer];
+      const size_t co = static_cast<size_t>(b0) * c.n_heads * c.max_seq * hd * m->esz;
+      da.kc = static_cast<char*>(m->kc[cur_layer]) + co;
+      da.vc = static_cast<char*>(m->vc[cur_layer]) + co;
       launch_decode_attention(da, s);
       const double keys = static_cast<double>(B) * c.max_seq;   // upper bound: full cache
       P(GM_K_ATTENTION, cur_layer, 4.0 * hd * keys * c.n_heads, es * 2.0 * keys * d);
@@ -578,7 +583,7 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
   }
   gemm(GM_K_GEMM_HEAD, z, d, m->head, c.vocab, kEpiStore, nullptr, lg, c.vocab, nullptr, -1);
   if (dec && dec->next) {
-    launch_argmax(lg, m->dtype, B, c.vocab, dec->next, s);
+    launch_argmax(lg, m->dtype, nb, c.vocab, dec->next + b0, s);
     P(GM_K_ARGMAX, -1, 0.0, es * B * static_cast<double>(c.vocab));
   }
   };
@@ -589,8 +594,9 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
   // whose per-element arithmetic does not depend on M, so the results are
   // the same bits as one branch.
   int parts = m->split_parts < B ? m->split_parts : B;
-  while (parts > 1 && (B / parts) * S <= 16) --parts;
-  if (dec || prof || c.fp16_clamp || c.log_hidden || c.kv_cache) parts = 1;
+  // (a decode step's parts run the skinny kernels, so any part size goes)
+  while (!dec && parts > 1 && (B / parts) * S <= 16) --parts;
+  if (prof || c.fp16_clamp || c.log_hidden || (c.kv_cache && !dec)) parts = 1;
   if (parts > 1) {
     // (the graph-broken run splits the same way: its only cut, the guards,
     // lies before the fork, and the fork and join go into the segment that
