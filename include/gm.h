@@ -249,7 +249,11 @@ void gm_model_destroy(gm_model *m);
  * start).  The buffers must stay valid until the stream reaches the end of
  * the forward.  Value errors go to the trap word (gm_check_error); the
  * logits of a trapped forward are unspecified but every access stays in
- * bounds. */
+ * bounds.  Part of the work (the second half of the batch, or of a decode
+ * step's sequences) runs on a stream the library owns, forked from `stream`
+ * with an event after the prologue and joined back with an event before the
+ * forward's last kernel: everything is complete once `stream` is.  Calls
+ * that overlap on one model race (they share its workspace). */
 int gm_forward(gm_model *m, const int32_t *token_ids, const int32_t *attn_mask,
                void *out_logits, hipStream_t stream);
 
