@@ -112,7 +112,7 @@ constexpr int kKB = 64;
 // transposed on the way into LDS, two keys at a time (4-byte LDS writes).
 // With a causal mask, query blocks run heaviest (last) first.  A wavefront
 // holds 16 U queries (U = 1: 64 queries per workgroup).
-template <typename T, int HD, int U>
+template <typename T, int HD, int U, int ORD>
 __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
   constexpr int QB = 64 * U;       // queries per workgroup: 4 wavefronts x 16U
   typedef typename MfmaA<T>::vec vec;
@@ -127,9 +127,26 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) T sK[2][kKB * LDK];
   __shared__ __attribute__((aligned(16))) T sVt[2][HD * LDV];
   __shared__ int sMask[2][kKB];
+  __shared__ int sFull[2];         // every key of the tile visible (no padding inside it)
   const int nqb = (a.Sq + QB - 1) / QB;
-  const int qb = a.causal ? nqb - 1 - static_cast<int>(blockIdx.x) : static_cast<int>(blockIdx.x);
-  const int h = blockIdx.y, b = blockIdx.z;
+  int qb, h, b;
+  if constexpr (ORD == 0) {
+    qb = a.causal ? nqb - 1 - static_cast<int>(blockIdx.x) : static_cast<int>(blockIdx.x);
+    h = blockIdx.y;
+    b = blockIdx.z;
+  } else {
+    const int P = a.B * a.H;
+    int p = blockIdx.x;
+    if constexpr (ORD == 2) {
+      constexpr int kSlot = 256;
+      const int sl = p / kSlot;
+      if ((sl & 1) && (sl + 1) * kSlot <= nqb * P) p = sl * kSlot + (kSlot - 1 - (p - sl * kSlot));
+    }
+    const int qi = p / P, pair = p - qi * P;
+    qb = a.causal ? nqb - 1 - qi : qi;
+    b = pair / a.H;
+    h = pair - b * a.H;
+  }
   const int Sq = a.Sq, S = a.Sk, d = a.d, ld = a.ldkv;
   const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
   const int l16 = lane & 15, g = lane >> 4;
@@ -213,7 +230,11 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
             *reinterpret_cast<const uint32_t*>(pair);
       }
     }
-    if (t < kKB) sMask[buf][t] = rm;
+    if (t < kKB) {                 // wavefront 0, all lanes
+      sMask[buf][t] = rm;
+      const unsigned long long all = __ballot(rm != 0);
+      if (t == 0) sFull[buf] = all == ~0ull;
+    }
   };
 
   if (kend > 0) gload(0);
@@ -239,22 +260,36 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
         for (int u = 0; u < U; ++u) sacc[kt][u] = MfmaA<T>::run(kf, qf[u][c], sacc[kt][u]);
       }
     }
-    // ---- masks and online softmax (per query = per (u, l16))
+    // ---- masks and online softmax (per query = per (u, l16)).  A tile with
+    // no padded key that lies wholly at or below this wavefront's first
+    // query needs no mask (the same scores, without the per-key tests).
+    const bool open = sFull[buf] && (!a.causal || kb + kKB - 1 <= q0);
     float p[4][U][4];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int qi = q0 + 16 * u + l16;
       float tmax = -INFINITY;
+      if (open) {
 #pragma unroll
-      for (int kt = 0; kt < 4; ++kt)
+        for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int kl = 16 * kt + 4 * g + r;
-          const bool ok = sMask[buf][kl] && (!a.causal || kb + kl <= qi);
-          const float s = ok ? sacc[kt][u][r] * sl2 : -INFINITY;
-          p[kt][u][r] = s;
-          tmax = fmaxf(tmax, s);
-        }
+          for (int r = 0; r < 4; ++r) {
+            const float s = sacc[kt][u][r] * sl2;
+            p[kt][u][r] = s;
+            tmax = fmaxf(tmax, s);
+          }
+      } else {
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int kl = 16 * kt + 4 * g + r;
+            const bool ok = sMask[buf][kl] && (!a.causal || kb + kl <= qi);
+            const float s = ok ? sacc[kt][u][r] * sl2 : -INFINITY;
+            p[kt][u][r] = s;
+            tmax = fmaxf(tmax, s);
+          }
+      }
       tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
       tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
       const float mnew = fmaxf(mrow[u], tmax);
@@ -323,7 +358,20 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
 }
 
 static bool g_attn_rows = false;
+static int g_attn_order = 2;
 void attention_force_rows(bool on) { g_attn_rows = on; }
+void attention_set_order(int o) { g_attn_order = o; }
+
+template <int U, int ORD>
+static void launch_attn_ord(const AttnArgs& a, dim3 grid, hipStream_t s) {
+  if (a.dtype == kBF16) {
+    if (a.hd == 64) hipLaunchKernelGGL((k_attn_mfma<bf16_t, 64, U, ORD>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((k_attn_mfma<bf16_t, 128, U, ORD>), grid, dim3(256), 0, s, a);
+  } else {
+    if (a.hd == 64) hipLaunchKernelGGL((k_attn_mfma<f16_t, 64, U, ORD>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((k_attn_mfma<f16_t, 128, U, ORD>), grid, dim3(256), 0, s, a);
+  }
+}
 
 void launch_attention(const AttnArgs& a, hipStream_t s) {
   const bool mfma_ok = a.dtype != kF32 && (a.hd == 64 || a.hd == 128) && !g_attn_rows;
@@ -340,13 +388,14 @@ void launch_attention(const AttnArgs& a, hipStream_t s) {
   // is a dependent chain (scores, masked online softmax, P.V) that needs
   // other wavefronts to hide its latency
   constexpr int U = 1;
-  const dim3 grid((a.Sq + 64 * U - 1) / (64 * U), a.H, a.B);
-  if (a.dtype == kBF16) {
-    if (a.hd == 64) hipLaunchKernelGGL((k_attn_mfma<bf16_t, 64, U>), grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((k_attn_mfma<bf16_t, 128, U>), grid, dim3(256), 0, s, a);
+  const int nqb = (a.Sq + 64 * U - 1) / (64 * U);
+  if (g_attn_order == 0) {
+    const dim3 grid(nqb, a.H, a.B);
+    launch_attn_ord<U, 0>(a, grid, s);
   } else {
-    if (a.hd == 64) hipLaunchKernelGGL((k_attn_mfma<f16_t, 64, U>), grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((k_attn_mfma<f16_t, 128, U>), grid, dim3(256), 0, s, a);
+    const dim3 grid(nqb * a.H * a.B);
+    if (g_attn_order == 1) launch_attn_ord<U, 1>(a, grid, s);
+    else launch_attn_ord<U, 2>(a, grid, s);
   }
 }
 

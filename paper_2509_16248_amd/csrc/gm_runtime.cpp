@@ -18,6 +18,7 @@ namespace gm {
 void gemm_force_simple(bool on);
 void gemm_set_variant(int v);
 void attention_force_rows(bool on);
+void attention_set_order(int o);
 }
 
 using namespace gm;
@@ -992,6 +993,7 @@ int gm_model_create(const gm_config* cfg, const gm_weights* w, gm_model** out) {
   gemm_force_simple(getenv("GM_SIMPLE_GEMM") && atoi(getenv("GM_SIMPLE_GEMM")));
   gemm_set_variant(getenv("GM_GEMM_VARIANT") ? atoi(getenv("GM_GEMM_VARIANT")) : 0);
   attention_force_rows(getenv("GM_SIMPLE_ATTN") && atoi(getenv("GM_SIMPLE_ATTN")));
+  attention_set_order(getenv("GM_ATTN_ORDER") ? atoi(getenv("GM_ATTN_ORDER")) : 2);
   auto fail = [&](int code) {
     gm_model_destroy(m);
     return code;
