@@ -196,9 +196,9 @@ __device__ __forceinline__ void site_flush(const GemmArgs& a, SiteMax& sm) {
 // ------------------------------------------------------------ MFMA 32x32 kernel
 constexpr int kBK = 64, kLDK = kBK + 8;   // K step; padded LDS row (elements)
 
-// Workgroup tile BM x BN (256 x 256 or 128 x 128), K step 64, 4 wavefronts
-// in a 2 x 2 grid; each wavefront owns (BM/2) x (BN/2) as TM x TN tiles of
-// v_mfma_f32_32x32x16 (bf16/f16 in, fp32 accumulate).  W is the MFMA A
+// Workgroup tile BM x BN, K step 64, WGM x WGN wavefronts; each wavefront
+// owns (BM/WGM) x (BN/WGN) as TM x TN tiles of v_mfma_f32_32x32x16 (bf16/f16
+// in, fp32 accumulate).  W is the MFMA A
 // operand and the activations the B operand: a lane ends up with the output
 // columns n = 32j + 8q + 4(lane/32) + r (q, r = 0..3) of row
 // m = 32i + lane%32, so the columns of a 16-row weight group (q = 0, 1) and
@@ -261,8 +261,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm_x(GemmArgs a) {
   static_assert(BM % RPP == 0 && BN % RPP == 0, "tile rows must split evenly");
   static_assert(TM >= 1 && TN >= 1, "wavefront tile below 32x32");
   constexpr int LDS_OPS = 2 * (BM + BN) * kLDK * static_cast<int>(sizeof(T));
-  constexpr int LDC = BN + 4;                   // fp32 staging row pitch
-  constexpr bool STAGE = BM * LDC * 4 <= LDS_OPS;
+  constexpr bool STAGE = BM * (BN + 8) * static_cast<int>(sizeof(T)) <= LDS_OPS;  // output-type staging tile
   __shared__ __attribute__((aligned(16))) char smem[LDS_OPS];
   T (*sA)[BM * kLDK] = reinterpret_cast<T (*)[BM * kLDK]>(smem);
   T (*sB)[BN * kLDK] = reinterpret_cast<T (*)[BN * kLDK]>(smem + 2 * BM * kLDK * sizeof(T));
@@ -376,79 +375,87 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm_x(GemmArgs a) {
 
   SiteMax sm;
   if (STAGE && !a.kc && (a.epi == kEpiStore || a.epi == kEpiGelu || a.epi == kEpiResid)) {
-    // Column-independent epilogues go through LDS: bias (and GELU) are
-    // applied in registers, the fp32 tile is staged, and rows are then
-    // written by consecutive lanes on consecutive columns: 16-byte chunks
-    // when output (and residual) rows are 16-byte aligned, single elements
-    // otherwise (the odd vocabulary of the head).
-    float* st = reinterpret_cast<float*>(smem);
+    // Column-independent epilogues finish in registers (bias, then GELU or
+    // the residual, one rounding to the output type, the site statistics
+    // of the rounded values) and stage the tile in LDS in the output type;
+    // rows then leave with consecutive lanes on consecutive columns: 16-byte
+    // chunks when output rows are 16-byte aligned, single elements otherwise
+    // (the odd vocabulary of the head).
+    constexpr int LDB = BN + 8;
+    T* stb = reinterpret_cast<T*>(smem);
     const T* bias = static_cast<const T*>(a.bias);
+    const bool bias8 = (reinterpret_cast<uintptr_t>(bias) & 7) == 0;
     T* out = static_cast<T*>(a.out);
-    const T* res = static_cast<const T*>(a.resid);
     const bool resid = a.epi == kEpiResid;
-    const bool aligned = (a.ldo & 7) == 0 && (!resid || (a.ldr & 7) == 0);
+    const T* res = static_cast<const T*>(a.resid);
+    const bool res8 = resid && (a.ldr & 3) == 0 && (reinterpret_cast<uintptr_t>(res) & 7) == 0;
     static_for<0, TM>([&](auto i) {
       const int ml = wm * WTM + 32 * i + l32;
+      const int m = bm + ml;
       static_for<0, TN>([&](auto j) {
         static_for<0, 4>([&](auto q) {
           const int nl = wn * WTN + 32 * j + 8 * q + 4 * g;
+          const int n0 = bn + nl;
           float v[4];
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            v[r] = acc[i][j][4 * q + r];
-            const int n = bn + nl + r;
-            if (bias && n < a.N) v[r] += to_f32(bias[n]);
-            if (a.epi == kEpiGelu) v[r] = gelu_f(v[r]);
+          for (int r = 0; r < 4; ++r) v[r] = acc[i][j][4 * q + r];
+          if (bias) {
+            if (bias8 && n0 + 4 <= a.N) {
+              const u32x2 bb = *reinterpret_cast<const u32x2*>(bias + n0);
+              const T* be = reinterpret_cast<const T*>(&bb);
+#pragma unroll
+              for (int r = 0; r < 4; ++r) v[r] += to_f32(be[r]);
+            } else {
+#pragma unroll
+              for (int r = 0; r < 4; ++r)
+                if (n0 + r < a.N) v[r] += to_f32(bias[n0 + r]);
+            }
           }
-          *reinterpret_cast<f32x4v*>(&st[ml * LDC + nl]) = f32x4v{v[0], v[1], v[2], v[3]};
+          if (a.epi == kEpiGelu)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) v[r] = gelu_f(v[r]);
+          if (resid && m < a.M) {
+            const T* rrow = res + static_cast<long long>(m) * a.ldr + n0;
+            if (res8 && n0 + 4 <= a.N) {
+              const u32x2 rr = *reinterpret_cast<const u32x2*>(rrow);
+              const T* re = reinterpret_cast<const T*>(&rr);
+#pragma unroll
+              for (int r = 0; r < 4; ++r) v[r] += to_f32(re[r]);
+            } else {
+#pragma unroll
+              for (int r = 0; r < 4; ++r)
+                if (n0 + r < a.N) v[r] += to_f32(rrow[r]);
+            }
+          }
+          u32x2 w;
+          T* we = reinterpret_cast<T*>(&w);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) we[r] = from_f32<T>(v[r]);
+          if (resid && a.site >= 0 && m < a.M)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (n0 + r < a.N) sm.add(to_f32(we[r]));
+          *reinterpret_cast<u32x2*>(&stb[ml * LDB + nl]) = w;
         });
       });
     });
     __syncthreads();
-    if (aligned) {
+    if ((a.ldo & 7) == 0) {
       constexpr int CPR = BN / 8;
       const int ncol = a.N - bn < BN ? a.N - bn : BN;
       for (int e = t; e < BM * CPR; e += NT) {
-        const int ml = e / CPR, k = e % CPR;
+        const int ml = e / CPR, j0 = 8 * (e % CPR);
         const int m = bm + ml;
-        const int j0 = 8 * k;
         if (m >= a.M || j0 >= ncol) continue;
-        const f32x4v lo = *reinterpret_cast<const f32x4v*>(&st[ml * LDC + 8 * k]);
-        const f32x4v hi = *reinterpret_cast<const f32x4v*>(&st[ml * LDC + 8 * k + 4]);
-        float v[8];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          v[r] = lo[r];
-          v[4 + r] = hi[r];
-        }
+        const u32x4 w = *reinterpret_cast<const u32x4*>(&stb[ml * LDB + j0]);
         T* orow = out + static_cast<long long>(m) * a.ldo + bn;
         if (j0 + 8 <= ncol) {
-          if (resid) {
-            const u32x4 rr = *reinterpret_cast<const u32x4*>(res + static_cast<long long>(m) * a.ldr + bn + j0);
-            const T* re = reinterpret_cast<const T*>(&rr);
-#pragma unroll
-            for (int r = 0; r < 8; ++r) v[r] += to_f32(re[r]);
-          }
-          u32x4 w;
-          T* we = reinterpret_cast<T*>(&w);
-#pragma unroll
-          for (int r = 0; r < 8; ++r) {
-            we[r] = from_f32<T>(v[r]);
-            if (resid && a.site >= 0) sm.add(to_f32(we[r]));
-          }
           *reinterpret_cast<u32x4*>(orow + j0) = w;
         } else {
-          // last chunk of a partial tile
+          const T* we = reinterpret_cast<const T*>(&w);
 #pragma unroll
-          for (int r = 0; r < 8; ++r) {
-            const int jj = j0 + r;
-            if (jj >= ncol) continue;
-            float y = v[r];
-            if (resid) y += to_f32(res[static_cast<long long>(m) * a.ldr + bn + jj]);
-            const T o = from_f32<T>(y);
-            if (resid && a.site >= 0) sm.add(to_f32(o));
-            orow[jj] = o;
-          }
+          for (int r = 0; r < 8; ++r)
+            if (j0 + r < ncol) orow[j0 + r] = we[r];
         }
       }
     } else {
@@ -456,11 +463,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm_x(GemmArgs a) {
         const int ml = e / BN, nl = e % BN;
         const int m = bm + ml, n = bn + nl;
         if (m >= a.M || n >= a.N) continue;
-        float v = st[ml * LDC + nl];
-        if (resid) v += to_f32(res[static_cast<long long>(m) * a.ldr + n]);
-        const T y = from_f32<T>(v);
-        if (resid && a.site >= 0) sm.add(to_f32(y));
-        out[static_cast<long long>(m) * a.ldo + n] = y;
+        out[static_cast<long long>(m) * a.ldo + n] = stb[ml * LDB + nl];
       }
     }
   } else {
