@@ -293,3 +293,24 @@ def test_full_size_causal_lm_768_sampled_sequences():
     res = OracleModel(cfg, w).forward(ids, mask, rows=rows)
     check_logits(f64(out[rows]), res.logits_f64, cfg.dtype, "causal_lm_768 rows 0,5")
     check_decisions(m.decisions(), res, cfg)
+
+
+def test_attention_workgroup_orders_give_the_same_bits(monkeypatch):
+    """The attention kernel's workgroup order (the 3-D grid, or the
+    one-dimensional query-block-major order with or without every other run
+    of 256 workgroups reversed) only moves (query block, sequence, head)
+    items between workgroups, so the logits are the same bits.  8 x 512
+    causal with 12 heads in one batch part gives 768 workgroups per launch:
+    three runs of 256, the middle one reversed."""
+    cfg = synth.preset("causal_lm_768", n_layers=2, vocab=1000)
+    w = synth.make_weights(cfg, 61)
+    ids, mask = synth.make_inputs(cfg, 9)
+    monkeypatch.setenv("GM_SPLIT_PARTS", "1")
+    outs = []
+    for order in (0, 1, 2):        # 2, the default, last: the setting is process-wide
+        monkeypatch.setenv("GM_ATTN_ORDER", str(order))
+        outs.append(run(gpu_model(cfg, w), ids, mask))
+    for o in outs[1:]:
+        assert torch.equal(o.view(torch.int16), outs[0].view(torch.int16))
+    res = OracleModel(cfg, w).forward(ids, mask, rows=[3])
+    check_logits(f64(outs[2][[3]]), res.logits_f64, cfg.dtype, "row 3")
