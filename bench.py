@@ -271,7 +271,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU (got --gpus {args.gpus}); "
-              "the multi-GPU layout is described in DESIGN.md, not built", file=sys.stderr)
+              "the multi-GPU layout is a design only, not built", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
