@@ -286,14 +286,31 @@ __global__ __launch_bounds__(1024) void k_argmax(const T* __restrict__ logits, i
   const T* row = logits + static_cast<long long>(blockIdx.x) * V;
   float best = -INFINITY;
   int bi = 0x7FFFFFFF, ni = 0x7FFFFFFF;
-  for (int i = threadIdx.x; i < V; i += blockDim.x) {
-    const float v = to_f32(row[i]);
+  auto visit = [&](float v, int i) {
     if (v != v) ni = min(ni, i);
     else if (v > best || (v == best && i < bi)) {
       best = v;
       bi = i;
     }
+  };
+  // Rows of odd length start anywhere: scalar loads up to the first 16-byte
+  // boundary, then 16-byte vectors (several in flight per thread), then the
+  // scalar tail.  The visiting order does not matter: ties go to the
+  // smaller index either way.
+  constexpr int VN = 16 / static_cast<int>(sizeof(T));
+  int head = static_cast<int>(((16 - (reinterpret_cast<uintptr_t>(row) & 15)) & 15) / sizeof(T));
+  head = head < V ? head : V;
+  for (int i = threadIdx.x; i < head; i += blockDim.x) visit(to_f32(row[i]), i);
+  const int nvec = (V - head) / VN;
+  const u32x4* vrow = reinterpret_cast<const u32x4*>(row + head);
+#pragma unroll 4
+  for (int j = threadIdx.x; j < nvec; j += blockDim.x) {
+    const u32x4 raw = vrow[j];
+    const T* e = reinterpret_cast<const T*>(&raw);
+#pragma unroll
+    for (int k = 0; k < VN; ++k) visit(to_f32(e[k]), head + j * VN + k);
   }
+  for (int i = head + nvec * VN + threadIdx.x; i < V; i += blockDim.x) visit(to_f32(row[i]), i);
   for (int o = 32; o > 0; o >>= 1) {
     const float v2 = __shfl_xor(best, o, 64);
     const int i2 = __shfl_xor(bi, o, 64);
