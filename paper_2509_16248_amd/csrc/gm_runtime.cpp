@@ -386,6 +386,9 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
   P(GM_K_EMBED, -1, 0.0, static_cast<double>(T) * d * es * (c.pos == GM_POS_LEARNED ? 3 : 2));
   r.ids = nullptr;
 
+  // a decode step's head runs once over the whole batch after the join (one
+  // pass over the head's weights instead of one per part)
+  bool head_joined = false;
   // The layers and the head over sequences [b0, b0 + nb) on stream s.
   auto layers_and_head = [&](hipStream_t s, int b0, int nb) {
   const int T = nb * S;
@@ -584,6 +587,7 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
     norm_rows(hh, aa, m->lnf_g, m->lnf_b, prev_site);
     z = aa;
   }
+  if (head_joined) return;
   gemm(GM_K_GEMM_HEAD, z, d, m->head, c.vocab, kEpiStore, nullptr, lg, c.vocab, nullptr, -1);
   if (dec && dec->next) {
     launch_argmax(lg, m->dtype, nb, c.vocab, dec->next + b0, s);
@@ -592,14 +596,15 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
   };
   // Independent batch-part branches (fork/join on auxiliary streams) where
   // nothing couples the sequences inside the layers: no clamp (its decision
-  // is batch-global), no tensor log, no KV cache, not a decode step or
-  // profile, and every part large enough for the tiled GEMMs,
-  // whose per-element arithmetic does not depend on M, so the results are
-  // the same bits as one branch.
+  // is batch-global), no tensor log, not a KV-cache prefill or a profile,
+  // and every forward part large enough for the tiled GEMMs, whose
+  // per-element arithmetic does not depend on M, so the results are the same
+  // bits as one branch.
   int parts = m->split_parts < B ? m->split_parts : B;
   // (a decode step's parts run the skinny kernels, so any part size goes)
   while (!dec && parts > 1 && (B / parts) * S <= 16) --parts;
   if (prof || c.fp16_clamp || c.log_hidden || (c.kv_cache && !dec)) parts = 1;
+  head_joined = parts > 1 && dec;
   if (parts > 1) {
     // (the graph-broken run splits the same way: its only cut, the guards,
     // lies before the fork, and the fork and join go into the segment that
@@ -617,6 +622,27 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
         (void)hipEventRecord(m->ev_join[i], m->aux_stream[i]);
         (void)hipStreamWaitEvent(s, m->ev_join[i], 0);
       }
+    if (head_joined) {
+      GemmArgs q{};
+      q.dtype = m->dtype;
+      q.M = B;
+      q.N = c.vocab;
+      q.K = d;
+      q.A = pre ? m->a : m->h;   // the final norm's output, or the stream itself
+      q.lda = d;
+      q.W = m->head;
+      q.ldw = d;
+      q.epi = kEpiStore;
+      q.out = logits;
+      q.ldo = c.vocab;
+      q.state = m->state;
+      q.site = -1;
+      q.seq = S;
+      q.head_dim = hd;
+      q.d_model = d;
+      launch_gemm(q, s);
+      if (dec->next) launch_argmax(logits, m->dtype, B, c.vocab, dec->next, s);
+    }
   } else {
     layers_and_head(s, 0, B);
   }
