@@ -252,7 +252,8 @@ void gm_model_destroy(gm_model *m);
  * bounds.  Part of the work (the second half of the batch, or of a decode
  * step's sequences) runs on a stream the library owns, forked from `stream`
  * with an event after the prologue and joined back with an event before the
- * forward's last kernel: everything is complete once `stream` is.  Calls
+ * forward's closing kernels (a decode step: before its LM head, which runs
+ * once over all rows): everything is complete once `stream` is.  Calls
  * that overlap on one model race (they share its workspace). */
 int gm_forward(gm_model *m, const int32_t *token_ids, const int32_t *attn_mask,
                void *out_logits, hipStream_t stream);
