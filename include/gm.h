@@ -225,7 +225,10 @@ typedef struct gm_stats {
 
 /* ------------------------------------------------------------ entry points */
 
-/* Create a model on the current device: validate cfg (host checks of shapes
+/* Paper: the Predicated Trap Lowering Transformation (host checks of tensor
+ * metadata stay on the host, value checks move to the device) and the
+ * hoisted, memoised initialisation of the Semantics Preservation section.
+ * Create a model on the current device: validate cfg (host checks of shapes
  * and dtypes, the static half of [Trap]), allocate weights, workspace for
  * max_batch x max_seq tokens and device state, copy and repack the weights,
  * build rotary rows [0, rope_init_len).  Synchronous.  On success *out owns
@@ -237,7 +240,11 @@ int gm_model_create(const gm_config *cfg, const gm_weights *w, gm_model **out);
  * is ignored. */
 void gm_model_destroy(gm_model *m);
 
-/* Enqueue one forward over [max_batch, max_seq] tokens on `stream`.
+/* Paper: Table "GraphMend transformation rules" ([Trap], [Where], [Defer]
+ * applied to the forward) and Evaluation, "Overhead Analysis of Graph
+ * Breaks" (the mended forward runs as one continuous graph with no CPU-GPU
+ * synchronisation) and "Full-Graph Capture for Serving Frameworks".
+ * Enqueue one forward over [max_batch, max_seq] tokens on `stream`.
  *  token_ids  device int32 [B, S] row-major, each in [0, vocab)
  *  attn_mask  device int32 [B, S] row-major, 1 = token, 0 = padding
  *  out_logits device [B, S, vocab] in act_dtype, row-major
@@ -258,14 +265,19 @@ void gm_model_destroy(gm_model *m);
 int gm_forward(gm_model *m, const int32_t *token_ids, const int32_t *attn_mask,
                void *out_logits, hipStream_t stream);
 
-/* As gm_forward over B <= max_batch sequences of S <= max_seq tokens.  With
+/* Paper: as gm_forward (the transformation rules table; Evaluation,
+ * "Overhead Analysis of Graph Breaks"), for any batch and sequence length.
+ * As gm_forward over B <= max_batch sequences of S <= max_seq tokens.  With
  * kv_cache it also stores every position's k and v (with its mask value) and
  * sets the length of sequence b to 1 + its last unmasked position: the
  * prefill that gm_decode_step continues. */
 int gm_forward_ex(gm_model *m, int32_t B, int32_t S, const int32_t *token_ids,
                   const int32_t *attn_mask, void *out_logits, hipStream_t stream);
 
-/* One decode step (kv_cache models): append token_ids[b] to sequence b at
+/* Paper: Evaluation, "Experimental Setup" (text models generate greedily
+ * token by token) and "Throughput Improvement"; the rotary-cache regrow of
+ * the Motivation's Phi-4 example fires mid-generation (rule [Where]).
+ * One decode step (kv_cache models): append token_ids[b] to sequence b at
  * position p_b = its current length, run the layer stack on those B rows
  * with attention over the cached keys 0..p_b (keys the prefill masked stay
  * masked), and write the logits of the new positions.  The result equals the
@@ -287,7 +299,9 @@ int gm_forward_ex(gm_model *m, int32_t B, int32_t S, const int32_t *token_ids,
 int gm_decode_step(gm_model *m, int32_t B, const int32_t *token_ids, void *out_logits,
                    int32_t *next_ids, hipStream_t stream);
 
-/* Encoder-decoder forward (n_dec_layers > 0): the encoder over
+/* Paper: Evaluation, "Benchmark Suite" (encoder-decoder text models) with
+ * the rules [Trap], [Where] and [Defer] applied to each of the two inputs.
+ * Encoder-decoder forward (n_dec_layers > 0): the encoder over
  * src_ids/src_mask [B, S_src] (S_src <= max_seq), then the decoder over
  * tgt_ids/tgt_mask [B, S_tgt] (S_tgt <= max_tgt) attending to the encoder
  * output; out_logits [B, S_tgt, vocab].  Device int32 inputs, 16-byte
@@ -302,7 +316,9 @@ int gm_forward_seq2seq(gm_model *m, int32_t B, int32_t S_src, const int32_t *src
                        const int32_t *src_mask, int32_t S_tgt, const int32_t *tgt_ids,
                        const int32_t *tgt_mask, void *out_logits, hipStream_t stream);
 
-/* Run one forward without a graph, recording a HIP event on `stream` after
+/* Paper: Evaluation, "Profiling Methodology" (per-kernel attribution of
+ * forward time).
+ * Run one forward without a graph, recording a HIP event on `stream` after
  * every kernel, wait for it, and write one gm_kernel_time per launch (in
  * launch order) to out[0 .. min(cap, *n_out)).  Same kernels and results as
  * gm_forward_ex; synchronises `stream`, so it is a profiling call, not a
@@ -311,7 +327,10 @@ int gm_profile_forward(gm_model *m, int32_t B, int32_t S, const int32_t *token_i
                        const int32_t *attn_mask, void *out_logits, hipStream_t stream,
                        gm_kernel_time *out, int32_t cap, int32_t *n_out);
 
-/* How gm_forward runs the same kernels (same results in every mode):
+/* Paper: Evaluation, "Experimental Setup" (one CUDA graph per fused region
+ * between breaks) and "Overhead Analysis of Graph Breaks" (a break costs a
+ * stream synchronisation, a device-to-host copy and host evaluation).
+ * How gm_forward runs the same kernels (same results in every mode):
  *  GM_EXEC_GRAPH (default)  one captured hipGraph per forward, no host sync;
  *  GM_EXEC_EAGER            kernels enqueued one by one, no host sync;
  *  GM_EXEC_FRAGMENTED       the unmended program the paper starts from: one
@@ -327,15 +346,21 @@ int gm_set_exec_mode(gm_model *m, int32_t mode);
 /* gm_set_exec_mode(m, enabled ? GM_EXEC_GRAPH : GM_EXEC_EAGER). */
 int gm_set_graph_mode(gm_model *m, int32_t enabled);
 
-/* Copy the decisions of the last forward enqueued on `stream` into *out.
+/* Paper: rule [Where] (Predicated Data-dependent Control Flow
+ * Transformation): the predicate values the original program's host `if`
+ * would have read, computed on the device.
+ * Copy the decisions of the last forward enqueued on `stream` into *out.
  * Synchronises `stream`; not for use inside a timed loop. */
 int gm_read_decisions(gm_model *m, gm_decisions *out, hipStream_t stream);
 
-/* Device address of the model's int32 decision slots, for zero-sync reads by
+/* Paper: rule [Where]; the predicate tensors stay on the device.
+ * Device address of the model's int32 decision slots, for zero-sync reads by
  * later kernels: [0] pad_any, [1] regrow, [2] need, [3] cached_len. */
 const int32_t *gm_decisions_device_ptr(const gm_model *m);
 
-/* Validation guard `if not torch.equal(attn_mask, expected): raise
+/* Paper: Predicated Validation Guards paragraph, Figure "guard_example",
+ * Predicated Trap Lowering Transformation.
+ * Validation guard `if not torch.equal(attn_mask, expected): raise
  * ValueError("unsupported attention mask")` on every later forward, lowered
  * as in rule [Trap]: the host checks the metadata (expected is int32 [B, S];
  * a forward of another shape fails the guard), the device checks
@@ -345,24 +370,32 @@ const int32_t *gm_decisions_device_ptr(const gm_model *m);
  * drops the cached graphs (they hold the previous guard). */
 int gm_set_mask_guard(gm_model *m, const int32_t *expected, int32_t B, int32_t S);
 
-/* The original exception of a trap code ("uid" of rule [Trap]): its Python
+/* Paper: Predicated Trap Lowering Transformation (the uid that maps a
+ * device trap back to the original exception).
+ * The original exception of a trap code ("uid" of rule [Trap]): its Python
  * type name and message, for the caller to raise when gm_check_error
  * reports the code.  Static strings. */
 int gm_trap_info(int32_t code, const char **exception_type, const char **message);
 
-/* Return and clear the sticky trap word: *code = GM_TRAP_* of the first
+/* Paper: rule [Trap]: a failed guard is reported at the next
+ * synchronisation point (Predicated Trap Lowering Transformation).
+ * Return and clear the sticky trap word: *code = GM_TRAP_* of the first
  * failing guard of the first trapped forward since the last call, *index =
  * row-major position of the first offending element (0 for the rotary
  * capacity).  Synchronises the device. */
 int gm_check_error(gm_model *m, int32_t *code, int32_t *index);
 
-/* Replay the deferred effect records in FIFO order through cb (which may be
+/* Paper: rule [Defer] (Deferred Side Effect Transformation): effects are
+ * recorded with their arguments during the graph and replayed in FIFO order
+ * after it.
+ * Replay the deferred effect records in FIFO order through cb (which may be
  * NULL to discard them) and empty the buffer.  *n_dropped (may be NULL)
  * receives the number of records lost to overflow since the last flush.
  * Synchronises the device. */
 int gm_flush_effects(gm_model *m, gm_effect_cb cb, void *user, int32_t *n_dropped);
 
-/* Device address and size in bytes of an internal activation buffer, for
+/* No passage: inspection plumbing for tests.
+ * Device address and size in bytes of an internal activation buffer, for
  * inspection after the stream has completed a forward (debugging and
  * tests).  which: 0 residual stream h [T, d], 1 norm output [T, d],
  * 2 fused q|k|v [T, 3d], 3 attention context [T, d], 4 FFN hidden [T, d_ff]
@@ -370,7 +403,10 @@ int gm_flush_effects(gm_model *m, gm_effect_cb cb, void *user, int32_t *n_droppe
  * last kernel that wrote the buffer. */
 int gm_debug_buffer(const gm_model *m, int32_t which, void **ptr, uint64_t *bytes);
 
-/* Host counters (no device access). */
+/* Paper: Evaluation, "Overhead Analysis of Graph Breaks" and "Steady-State
+ * Forward Pass Speedup": the counters show what a forward costs on the host
+ * (graph launches; sync-class HIP calls, which must stay 0 in a forward).
+ * Host counters (no device access). */
 int gm_get_stats(const gm_model *m, gm_stats *out);
 
 /* Static description of a return code, and the last HIP error message of

@@ -357,9 +357,7 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
   }
 }
 
-static bool g_attn_rows = false;
 static int g_attn_order = 2;
-void attention_force_rows(bool on) { g_attn_rows = on; }
 void attention_set_order(int o) { g_attn_order = o; }
 
 template <int U, int ORD>
@@ -374,7 +372,7 @@ static void launch_attn_ord(const AttnArgs& a, dim3 grid, hipStream_t s) {
 }
 
 void launch_attention(const AttnArgs& a, hipStream_t s) {
-  const bool mfma_ok = a.dtype != kF32 && (a.hd == 64 || a.hd == 128) && !g_attn_rows;
+  const bool mfma_ok = a.dtype != kF32 && (a.hd == 64 || a.hd == 128);
   if (!mfma_ok) {
     const dim3 grid(a.Sq, a.H, a.B);
     const size_t lds = (a.hd + a.Sk) * sizeof(float);

@@ -486,238 +486,6 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm_x(GemmArgs a) {
   site_flush(a, sm);
 }
 
-// ------------------------------------------------------------ LDS-DMA kernel
-// Same tiling and epilogues as k_gemm_x, but operand tiles travel from global
-// memory straight into LDS with global_load_lds_dwordx4 (no register
-// staging), through a ring of NS LDS stages: NS-1 K steps are in flight while
-// one is multiplied.  One wavefront instruction fills 1 KB of LDS, lane i at
-// byte 16*i, i.e. 8 tile rows of 128 bytes; the lane chooses which 16-byte
-// chunk of its row it fetches so that row r's chunk c lands in slot
-// c ^ ((r >> 1) & 7).  LDS serves a 16-byte read for 16 lanes at a time
-// from 64 four-byte banks (256 bytes, two tile rows): with this swizzle the
-// 16 consecutive rows an MFMA operand read touches at a time fall on 16
-// distinct 16-byte bank groups.  Waits are explicit (s_waitcnt vmcnt + s_barrier); the
-// compiler does not track the DMA writes.
-typedef __attribute__((address_space(3))) void* lds_ptr_t;
-
-// 16 bytes per lane, global -> LDS (lane i lands at lds + 16*i)
-__device__ __forceinline__ void dma16(const void* g, void* lds) {
-  __builtin_amdgcn_global_load_lds(g, (lds_ptr_t)lds, 16, 0, 0);
-}
-
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
-}
-
-template <typename T, int BM, int BN, int WGM, int WGN, int NS>
-__global__ __launch_bounds__(64 * WGM * WGN) void k_gemm_dma(GemmArgs a) {
-  typedef typename Mfma32<T>::vec vec;
-  constexpr int NW = WGM * WGN, NT = 64 * NW;
-  constexpr int WTM = BM / WGM, WTN = BN / WGN;
-  constexpr int TM = WTM / 32, TN = WTN / 32;
-  constexpr int KS = kBK / 16;
-  constexpr int STAGE_ELEMS = (BM + BN) * kBK;              // one stage, A then B
-  constexpr int LPS = (BM + BN) / 8 / NW;                   // DMA instructions per wave per stage
-  constexpr int LDS_OPS = NS * STAGE_ELEMS * static_cast<int>(sizeof(T));
-  constexpr int LDC = BN + 4;
-  constexpr bool STAGE = BM * LDC * 4 <= LDS_OPS;
-  static_assert((BM + BN) % (8 * NW) == 0, "stage rows must split over the wavefronts");
-  static_assert(kBK * sizeof(T) == 128, "a tile row must be 128 bytes");
-  __shared__ __attribute__((aligned(1024))) char smem[LDS_OPS];
-  T* lds = reinterpret_cast<T*>(smem);
-  const int tiles_m = (a.M + BM - 1) / BM, tiles_n = (a.N + BN - 1) / BN;
-  int tm, tn;
-  tile_of(blockIdx.x, tiles_m, tiles_n, tm, tn);
-  const int bm = tm * BM, bn = tn * BN;
-  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
-  const T* __restrict__ A0 = static_cast<const T*>(a.A);
-  const T* __restrict__ W0 = static_cast<const T*>(a.W);
-
-  // this lane's source rows for its LPS instructions: stage row
-  // sr = (wave * LPS + j) * 8 + lane / 8; rows < BM are A rows, the rest W rows
-  const T* src[LPS];
-#pragma unroll
-  for (int j = 0; j < LPS; ++j) {
-    const int sr = (wave * LPS + j) * 8 + (lane >> 3);
-    const int chunk = (lane & 7) ^ ((sr >> 1) & 7);
-    if (sr < BM) {
-      int r = bm + sr;
-      r = r < a.M ? r : a.M - 1;
-      src[j] = A0 + static_cast<long long>(r) * a.lda + chunk * 8;
-    } else {
-      int c = bn + sr - BM;
-      c = c < a.N ? c : a.N - 1;
-      src[j] = W0 + static_cast<long long>(c) * a.ldw + chunk * 8;
-    }
-  }
-  auto issue = [&](int stage_buf, int k0) {
-#pragma unroll
-    for (int j = 0; j < LPS; ++j) {
-      T* dst = lds + stage_buf * STAGE_ELEMS + (wave * LPS + j) * 8 * kBK;
-      dma16(src[j] + k0, dst);
-    }
-  };
-
-  const int wm = wave / WGN, wn = wave % WGN;
-  const int l32 = lane & 31, g = lane >> 5;
-  f32x16 acc[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
-
-  // Fragment reads: row r's 16-byte chunk c sits in slot c ^ ((r >> 1) & 7);
-  // (r >> 1) & 7 only depends on the lane (rows differ by multiples of 32).
-  const int swz = (l32 >> 1) & 7;
-  const int offA = (wm * WTM + l32) * kBK, offB = BM * kBK + (wn * WTN + l32) * kBK;
-  vec fa[2][TM], fb[2][TN];
-  auto read_frags = [&](auto set, const T* st, int ks) {
-    const int col = ((2 * ks + g) ^ swz) << 3;
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-      fb[set][j] = *reinterpret_cast<const vec*>(st + offB + 32 * j * kBK + col);
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-      fa[set][i] = *reinterpret_cast<const vec*>(st + offA + 32 * i * kBK + col);
-  };
-  // One stage: the fragments of k-step ks + 1 are read while the MFMAs of
-  // k-step ks run (the scheduler is told to alternate one MFMA with one LDS
-  // read), so LDS latency hides behind matrix work.
-  auto compute = [&](int stage_buf) {
-    const T* st = lds + stage_buf * STAGE_ELEMS;
-    read_frags(std::integral_constant<int, 0>{}, st, 0);
-    static_for<0, KS>([&](auto ks) {
-      constexpr int cur = decltype(ks)::value & 1;
-      if constexpr (decltype(ks)::value + 1 < KS)
-        read_frags(std::integral_constant<int, cur ^ 1>{}, st, decltype(ks)::value + 1);
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = Mfma32<T>::run(fb[cur][j], fa[cur][i], acc[i][j]);
-      if constexpr (decltype(ks)::value + 1 < KS) {
-        static_for<0, TM * TN>([&](auto q) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);      // one MFMA
-          if constexpr (decltype(q)::value < TM + TN)
-            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);    // one LDS read
-        });
-      }
-    });
-  };
-
-  const int nk = a.K / kBK;
-  static_for<0, NS - 1>([&](auto st) {
-    if (st < nk) issue(st, st * kBK);
-  });
-  for (int k = 0; k < nk; ++k) {
-    // stage k must have landed: allow the younger stages (up to NS-2) in flight
-    const int younger = nk - 1 - k < NS - 2 ? nk - 1 - k : NS - 2;
-    static_for<0, NS - 1>([&](auto y) {
-      if (y == younger) wait_vmcnt<LPS * decltype(y)::value>();
-    });
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-    if (k + NS - 1 < nk) issue((k + NS - 1) % NS, (k + NS - 1) * kBK);
-    compute(k % NS);
-  }
-  wait_vmcnt<0>();
-  __syncthreads();
-
-  SiteMax sm;
-  if (STAGE && !a.kc && (a.epi == kEpiStore || a.epi == kEpiGelu || a.epi == kEpiResid)) {
-    float* st = reinterpret_cast<float*>(smem);
-    const T* bias = static_cast<const T*>(a.bias);
-    static_for<0, TM>([&](auto i) {
-      const int ml = wm * WTM + 32 * i + l32;
-      static_for<0, TN>([&](auto j) {
-        static_for<0, 4>([&](auto q) {
-          const int nl = wn * WTN + 32 * j + 8 * q + 4 * g;
-          float v[4];
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            v[r] = acc[i][j][4 * q + r];
-            const int n = bn + nl + r;
-            if (bias && n < a.N) v[r] += to_f32(bias[n]);
-            if (a.epi == kEpiGelu) v[r] = gelu_f(v[r]);
-          }
-          *reinterpret_cast<f32x4v*>(&st[ml * LDC + nl]) = f32x4v{v[0], v[1], v[2], v[3]};
-        });
-      });
-    });
-    __syncthreads();
-    T* out = static_cast<T*>(a.out);
-    const T* res = static_cast<const T*>(a.resid);
-    const bool resid = a.epi == kEpiResid;
-    if ((a.ldo & 7) == 0 && (!resid || (a.ldr & 7) == 0) && bn + BN <= a.N) {
-      constexpr int CPR = BN / 8;
-      for (int e = t; e < BM * CPR; e += NT) {
-        const int ml = e / CPR, c = (e % CPR) * 8;
-        const int m = bm + ml;
-        if (m >= a.M) continue;
-        float v[8];
-        const f32x4v lo = *reinterpret_cast<const f32x4v*>(&st[ml * LDC + c]);
-        const f32x4v hi = *reinterpret_cast<const f32x4v*>(&st[ml * LDC + c + 4]);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          v[r] = lo[r];
-          v[4 + r] = hi[r];
-        }
-        if (resid) {
-          const u32x4 rr = *reinterpret_cast<const u32x4*>(res + static_cast<long long>(m) * a.ldr + bn + c);
-          const T* re = reinterpret_cast<const T*>(&rr);
-#pragma unroll
-          for (int r = 0; r < 8; ++r) v[r] += to_f32(re[r]);
-        }
-        u32x4 w;
-        T* we = reinterpret_cast<T*>(&w);
-#pragma unroll
-        for (int r = 0; r < 8; ++r) {
-          we[r] = from_f32<T>(v[r]);
-          if (resid && a.site >= 0) sm.add(to_f32(we[r]));
-        }
-        *reinterpret_cast<u32x4*>(out + static_cast<long long>(m) * a.ldo + bn + c) = w;
-      }
-    } else {
-      for (int e = t; e < BM * BN; e += NT) {
-        const int ml = e / BN, nl = e % BN;
-        const int m = bm + ml, n = bn + nl;
-        if (m >= a.M || n >= a.N) continue;
-        float v = st[ml * LDC + nl];
-        if (resid) v += to_f32(res[static_cast<long long>(m) * a.ldr + n]);
-        const T y = from_f32<T>(v);
-        if (resid && a.site >= 0) sm.add(to_f32(y));
-        out[static_cast<long long>(m) * a.ldo + n] = y;
-      }
-    }
-  } else {
-    static_for<0, TM>([&](auto i) {
-      const int m = bm + wm * WTM + 32 * i + l32;
-      static_for<0, TN>([&](auto j) {
-        static_for<0, 2>([&](auto q) {
-          const int nA = bn + wn * WTN + 32 * j + 8 * q + 4 * g;
-          float va[4], vb[4];
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            va[r] = acc[i][j][4 * q + r];
-            vb[r] = acc[i][j][4 * (q + 2) + r];
-          }
-          epi_pair<T>(a, m, nA, va, vb, sm);
-        });
-      });
-    });
-  }
-  site_flush(a, sm);
-}
-
-template <typename T, int BM, int BN, int WGM, int WGN, int NS>
-static void run_dma(const GemmArgs& a, hipStream_t s) {
-  const dim3 grid(((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN));
-  hipLaunchKernelGGL((k_gemm_dma<T, BM, BN, WGM, WGN, NS>), grid, dim3(64 * WGM * WGN), 0, s, a);
-}
-
 template <typename T, int BM, int BN, int WGM, int WGN, int PF>
 static void run_x(const GemmArgs& a, hipStream_t s) {
   const dim3 grid(((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN));
@@ -725,15 +493,7 @@ static void run_x(const GemmArgs& a, hipStream_t s) {
 }
 
 template <typename T>
-static void gemm_mfma(const GemmArgs& a, hipStream_t s, int variant) {
-  // alternative configurations kept for measurement (GM_GEMM_VARIANT)
-  switch (variant) {
-    case 12: run_x<T, 128, 128, 2, 4, 3>(a, s); return;
-    case 14: run_x<T, 128, 128, 2, 2, 2>(a, s); return;
-    case 24: run_dma<T, 256, 256, 2, 4, 2>(a, s); return;
-    case 27: run_dma<T, 128, 128, 2, 4, 2>(a, s); return;
-    default: break;
-  }
+static void gemm_mfma(const GemmArgs& a, hipStream_t s) {
   // 128 x 128 workgroup tiles, 8 wavefronts of 64 x 32, operands fetched two
   // K steps ahead (the best of the measured configurations on the projection
   // and head shapes).  Products too small to give the chip ~160 such tiles
@@ -1011,27 +771,20 @@ static void skinny_t(const GemmArgs& a, hipStream_t s) {
     skinny_r<T, 1>(a, s);
 }
 
-static bool g_force_simple = false;
-static int g_gemm_variant = 0;
-void gemm_force_simple(bool on) { g_force_simple = on; }
-void gemm_set_variant(int v) { g_gemm_variant = v; }
-
 void launch_gemm(const GemmArgs& a, hipStream_t s) {
-  if (a.M <= 16 && !g_force_simple) {
+  if (a.M <= 16) {
     if (a.dtype == kF32) skinny_t<float>(a, s);
     else if (a.dtype == kBF16) skinny_t<bf16_t>(a, s);
     else skinny_t<f16_t>(a, s);
     return;
   }
-  if (a.dtype == kF32 || g_force_simple) {
+  if (a.dtype == kF32) {
     const dim3 grid(((a.M + 63) / 64) * ((a.N + 63) / 64));
-    if (a.dtype == kF32) hipLaunchKernelGGL(k_gemm_simple<float>, grid, dim3(256), 0, s, a);
-    else if (a.dtype == kBF16) hipLaunchKernelGGL(k_gemm_simple<bf16_t>, grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL(k_gemm_simple<f16_t>, grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(k_gemm_simple<float>, grid, dim3(256), 0, s, a);
     return;
   }
-  if (a.dtype == kBF16) gemm_mfma<bf16_t>(a, s, g_gemm_variant);
-  else gemm_mfma<f16_t>(a, s, g_gemm_variant);
+  if (a.dtype == kBF16) gemm_mfma<bf16_t>(a, s);
+  else gemm_mfma<f16_t>(a, s);
 }
 
 }  // namespace gm

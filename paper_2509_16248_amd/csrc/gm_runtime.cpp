@@ -15,9 +15,6 @@
 #include "gm_kernels.h"
 
 namespace gm {
-void gemm_force_simple(bool on);
-void gemm_set_variant(int v);
-void attention_force_rows(bool on);
 void attention_set_order(int o);
 }
 
@@ -1018,9 +1015,6 @@ int gm_model_create(const gm_config* cfg, const gm_weights* w, gm_model** out) {
   m->esz = c.act_dtype == GM_DTYPE_F32 ? 4 : 2;
   memset(&m->stats, 0, sizeof(m->stats));
   m->debug_sync = getenv("GM_DEBUG_SYNC") && atoi(getenv("GM_DEBUG_SYNC"));
-  gemm_force_simple(getenv("GM_SIMPLE_GEMM") && atoi(getenv("GM_SIMPLE_GEMM")));
-  gemm_set_variant(getenv("GM_GEMM_VARIANT") ? atoi(getenv("GM_GEMM_VARIANT")) : 0);
-  attention_force_rows(getenv("GM_SIMPLE_ATTN") && atoi(getenv("GM_SIMPLE_ATTN")));
   attention_set_order(getenv("GM_ATTN_ORDER") ? atoi(getenv("GM_ATTN_ORDER")) : 2);
   auto fail = [&](int code) {
     gm_model_destroy(m);
