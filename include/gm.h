@@ -394,6 +394,27 @@ int gm_check_error(gm_model *m, int32_t *code, int32_t *index);
  * Synchronises the device. */
 int gm_flush_effects(gm_model *m, gm_effect_cb cb, void *user, int32_t *n_dropped);
 
+/* No passage: test instrumentation for per-layer parity.
+ * The forward of gm_forward_ex (pre-norm models), enqueued on `stream`
+ * without a graph and as one branch, copying every layer's storage points
+ * into `dump` (device, 16-byte aligned, at least
+ * n_layers * T * (8 * d_model + d_ff) elements of act_dtype, T = B * S):
+ * layer l's block starts at element l * T * (8d + ff) and holds, row-major,
+ *   a1 [T, d]     the first norm's output (with the preceding clamp site's
+ *                 select applied to the stream it reads),
+ *   qkv [T, 3d]   q | k | v after the projection epilogue (rotary applied),
+ *   ctx [T, d]    the attention context,
+ *   h_mid [T, d]  the stream after the attention residual (before the clamp
+ *                 site's select, which the next norm applies),
+ *   a2 [T, d]     the second norm's output,
+ *   f [T, ff]     the FFN hidden after the activation or gate product,
+ *   h_out [T, d]  the stream after the FFN residual (before its select).
+ * Asynchronous (no host sync); the logits, decisions and effects are those
+ * of an ordinary forward.  Not for the hot path. */
+int gm_debug_forward_layers(gm_model *m, int32_t B, int32_t S, const int32_t *token_ids,
+                            const int32_t *attn_mask, void *out_logits, hipStream_t stream,
+                            void *dump, uint64_t dump_bytes);
+
 /* No passage: inspection plumbing for tests.
  * Device address and size in bytes of an internal activation buffer, for
  * inspection after the stream has completed a forward (debugging and

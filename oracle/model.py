@@ -103,6 +103,21 @@ class OracleResult:
     rope_long: bool = False          # long/short rotary select: long factors used
 
 
+@dataclasses.dataclass
+class _Begin:
+    """State of a forward after its prologue (OracleModel.begin)."""
+    forward: int
+    effects: List[Effect]
+    pad_any: bool
+    regrow: bool
+    need: int
+    rope_long: bool
+    S: int
+    Br: int
+    allowed: np.ndarray   # [Br, 1, S, S] keys each query may attend to
+    h: np.ndarray         # [Br, S, d] embedding output (stored)
+
+
 def _cfg_get(cfg, name):
     return getattr(cfg, name)
 
@@ -171,6 +186,58 @@ class OracleModel:
         predicates (padding branch, rotary cache size) still read the full
         inputs, as the original program does.
         """
+        c = self.cfg
+        st = self.begin(ids, mask, force, rows, prefix)
+        force = force or {}
+        fwd, effects, h, allowed = st.forward, st.effects, st.h, st.allowed
+        pad_any, regrow, need, rope_long, Br = st.pad_any, st.regrow, st.need, st.rope_long, st.Br
+        S = st.S
+
+        clamp, absmaxes, nans, margins = [], [], [], []
+        for l in range(c.n_layers):
+            W = self._layer(l)
+            site_out = []
+            # ---------------- attention block
+            a = self.step_norm(h, W, 1) if c.norm_place == "pre" else h
+            q, k, v = self.step_qkv(a, W, S)
+            ctx = self.step_attention(q, k, v, allowed)
+            h, pre = self.step_residual(h, ctx, W["wo"], W.get("bo"))
+            if c.norm_place == "post":
+                h = self.step_norm(h, W, 1)
+            h, info = self._clamp_site(h, pre, l, 0, force, fwd, effects)
+            site_out.append(info)
+
+            # ---------------- feed-forward block
+            a = self.step_norm(h, W, 2) if c.norm_place == "pre" else h
+            f = self.step_ffn(a, W)
+            h, pre = self.step_residual(h, f, W["w2"], W.get("b2"))
+            if c.norm_place == "post":
+                h = self.step_norm(h, W, 2)
+            h, info = self._clamp_site(h, pre, l, 1, force, fwd, effects)
+            site_out.append(info)
+            if c.log_hidden:
+                # logger.info(..., h.abs().amax per sequence): the tensor is
+                # taken here; the original prints it at once
+                vals = tuple(float(v) for v in np.abs(h).reshape(Br, -1).max(axis=1))
+                effects.append(Effect(fwd, EFFECT_LOG, l, 0, float(Br), vals))
+            clamp.append((site_out[0][0], site_out[1][0]))
+            absmaxes.append((site_out[0][1], site_out[1][1]))
+            nans.append((site_out[0][2], site_out[1][2]))
+            margins.append((site_out[0][3], site_out[1][3]))
+
+        # --- head.
+        logits = self.step_head(h)
+        return OracleResult(
+            logits=nx.to_storage(logits, self.dt), logits_f64=logits,
+            pad_any=pad_any, regrow=regrow, need=need,
+            cached_len=self.cached_len, clamp=clamp, clamp_absmax=absmaxes,
+            clamp_nan=nans, clamp_margin=margins, effects=effects, rope_long=rope_long)
+
+    def begin(self, ids, mask, force: Optional[Dict] = None, rows: Optional[List[int]] = None,
+              prefix: Optional[int] = None) -> "_Begin":
+        """Everything before the first layer: the guards, the padding and
+        rotary branches (with their effects and the rotary state update),
+        the attention mask and the embedding output.  Counts a forward."""
         c = self.cfg
         force = force or {}
         fwd = self.forward_count
@@ -263,82 +330,98 @@ class OracleModel:
             h = self.R(self._norm(h, self._g("emb_ln_g"),
                                   self._g("emb_ln_b") if c.norm == "layernorm" else None))
 
-        clamp, absmaxes, nans, margins = [], [], [], []
-        d, H, hd = c.d_model, c.n_heads, c.head_dim
-        for l in range(c.n_layers):
-            W = self._layer(l)
-            site_out = []
-            # ---------------- attention block
-            a = self.R(self._norm(h, W["ln1_g"], W.get("ln1_b"))) if c.norm_place == "pre" else h
-            qkv = a @ W["wqkv"].T
-            if c.bias:
-                qkv = qkv + W["bqkv"]
-            q = qkv[..., :d].reshape(Br, S, H, hd).transpose(0, 2, 1, 3)
-            k = qkv[..., d:2 * d].reshape(Br, S, H, hd).transpose(0, 2, 1, 3)
-            v = qkv[..., 2 * d:].reshape(Br, S, H, hd).transpose(0, 2, 1, 3)
-            if c.pos == "rotary":
-                cos = self.rope_cos[:S]
-                sin = self.rope_sin[:S]
-                q = nx.apply_rope(q, cos, sin)
-                k = nx.apply_rope(k, cos, sin)
-            q, k, v = self.R(q), self.R(k), self.R(v)
-            s = (q @ k.transpose(0, 1, 3, 2)) * (1.0 / np.sqrt(hd))
-            p = nx.masked_softmax(s, allowed)
-            ctx = self.R(p @ v).transpose(0, 2, 1, 3).reshape(Br, S, d)
-            o = ctx @ W["wo"].T
-            if c.bias:
-                o = o + W["bo"]
-            pre = h + o
-            h = self.R(pre)
-            if c.norm_place == "post":
-                h = self.R(self._norm(h, W["ln1_g"], W.get("ln1_b")))
-            h, info = self._clamp_site(h, pre, l, 0, force, fwd, effects)
-            site_out.append(info)
+        return _Begin(forward=fwd, effects=effects, pad_any=pad_any, regrow=regrow, need=need,
+                      rope_long=rope_long, S=S, Br=Br, allowed=allowed, h=h)
 
-            # ---------------- feed-forward block
-            a = self.R(self._norm(h, W["ln2_g"], W.get("ln2_b"))) if c.norm_place == "pre" else h
-            u = a @ W["w1"].T
-            if c.bias:
-                u = u + W["b1"]
-            if c.gated:
-                ff = c.d_ff
-                g_, up = u[..., :ff], u[..., ff:]
-                act = nx.gelu(g_) if c.ffn == "geglu" else nx.silu(g_)
-                f = self.R(act * up)
-            else:
-                f = self.R(nx.gelu(u))
-            y = f @ W["w2"].T
-            if c.bias:
-                y = y + W["b2"]
-            pre = h + y
-            h = self.R(pre)
-            if c.norm_place == "post":
-                h = self.R(self._norm(h, W["ln2_g"], W.get("ln2_b")))
-            h, info = self._clamp_site(h, pre, l, 1, force, fwd, effects)
-            site_out.append(info)
-            if c.log_hidden:
-                # logger.info(..., h.abs().amax per sequence): the tensor is
-                # taken here; the original prints it at once
-                vals = tuple(float(v) for v in np.abs(h).reshape(Br, -1).max(axis=1))
-                effects.append(Effect(fwd, EFFECT_LOG, l, 0, float(Br), vals))
-            clamp.append((site_out[0][0], site_out[1][0]))
-            absmaxes.append((site_out[0][1], site_out[1][1]))
-            nans.append((site_out[0][2], site_out[1][2]))
-            margins.append((site_out[0][3], site_out[1][3]))
+    # ---------------------------------------------------------------- steps
+    # The steps of one layer, each from its stored input to its stored output
+    # (the storage points of the module docstring).  ``forward`` composes
+    # them; tests may also apply one step to a given input.
+    def layer_weights(self, l):
+        """Layer l's weights as float64 (nn.Linear layout)."""
+        return self._layer(l)
 
-        # --- head.
+    def step_norm(self, h, W, which):
+        """R(Norm(h)) with the layer's first (which=1) or second norm."""
+        return self.R(self._norm(h, W[f"ln{which}_g"], W.get(f"ln{which}_b")))
+
+    def step_qkv(self, a, W, S, positions=None):
+        """q, k, v = R(a Wqkv^T + b), split per head [B, H, S, hd], with the
+        rotary rotation of q and k (rotary models) before the rounding; the
+        rows' positions are 0..S-1, or ``positions`` [S]."""
+        c = self.cfg
+        H, hd, d = c.n_heads, c.head_dim, c.d_model
+        B = a.shape[0]
+        qkv = a @ W["wqkv"].T
+        if c.bias:
+            qkv = qkv + W["bqkv"]
+        q = qkv[..., :d].reshape(B, S, H, hd).transpose(0, 2, 1, 3)
+        k = qkv[..., d:2 * d].reshape(B, S, H, hd).transpose(0, 2, 1, 3)
+        v = qkv[..., 2 * d:].reshape(B, S, H, hd).transpose(0, 2, 1, 3)
+        if c.pos == "rotary":
+            pos = np.arange(S) if positions is None else np.asarray(positions)
+            cos = self.rope_cos[pos]
+            sin = self.rope_sin[pos]
+            q = nx.apply_rope(q, cos, sin)
+            k = nx.apply_rope(k, cos, sin)
+        return self.R(q), self.R(k), self.R(v)
+
+    def step_attention(self, q, k, v, allowed):
+        """ctx = R(softmax over allowed keys of q k^T / sqrt(hd)) v), heads
+        concatenated: [B, S, d]; a query with no allowed key gives 0."""
+        B, H, S, hd = q.shape
+        s = (q @ k.transpose(0, 1, 3, 2)) * (1.0 / np.sqrt(hd))
+        p = nx.masked_softmax(s, allowed)
+        return self.R(p @ v).transpose(0, 2, 1, 3).reshape(B, S, H * hd)
+
+    def step_residual(self, h, x, Wm, b):
+        """The residual add of a block: pre = h + x Wm^T (+ b); returns
+        (R(pre), pre)."""
+        o = x @ Wm.T
+        if b is not None and self.cfg.bias:
+            o = o + b
+        pre = h + o
+        return self.R(pre), pre
+
+    def step_ffn(self, a, W):
+        """f = R(gelu(a W1^T + b1)), or for gated FFNs R(act(a Wg^T) * (a Wu^T))
+        with the gate rows first in W1."""
+        c = self.cfg
+        u = a @ W["w1"].T
+        if c.bias:
+            u = u + W["b1"]
+        if c.gated:
+            ff = c.d_ff
+            g_, up = u[..., :ff], u[..., ff:]
+            act = nx.gelu(g_) if c.ffn == "geglu" else nx.silu(g_)
+            return self.R(act * up)
+        return self.R(nx.gelu(u))
+
+    def step_head(self, h):
+        """logits = R(Norm_f(h) W_head^T) (pre-norm; post-norm models read h)."""
+        c = self.cfg
         if c.norm_place == "pre":
             z = self.R(self._norm(h, self._g("lnf_g"),
                                   self._g("lnf_b") if c.norm == "layernorm" else None))
         else:
             z = h
         head = self._g("tok_emb") if c.tied_head else self._g("lm_head")
-        logits = self.R(z @ head.T)
-        return OracleResult(
-            logits=nx.to_storage(logits, self.dt), logits_f64=logits,
-            pad_any=pad_any, regrow=regrow, need=need,
-            cached_len=self.cached_len, clamp=clamp, clamp_absmax=absmaxes,
-            clamp_nan=nans, clamp_margin=margins, effects=effects, rope_long=rope_long)
+        return self.R(z @ head.T)
+
+    def clamp_decision(self, h):
+        """The fp16 overflow branch's predicate on a stored residual stream:
+        (trip, max |h| over the non-NaN elements, any NaN).  ``max``
+        propagates NaN, so a NaN anywhere makes the comparison false."""
+        thr = FP16_MAX - self.cfg.clamp_margin
+        has_nan = bool(np.isnan(h).any())
+        finite = h[~np.isnan(h)]
+        absmax = float(np.abs(finite).max(initial=0.0))
+        return (not has_nan) and absmax > thr, absmax, has_nan
+
+    def clamp_apply(self, h):
+        """Body of the clamp branch: R(clip(h, -thr, thr))."""
+        thr = FP16_MAX - self.cfg.clamp_margin
+        return self.R(np.clip(h, -thr, thr))
 
     def _clamp_site(self, h, pre, l, s, force, fwd, effects):
         """fp16 overflow guard after a residual add: ``if abs(h).max() >

@@ -249,6 +249,140 @@ __device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int& 
   tn = in / rows;
 }
 
+// Epilogue of one BM x BN output tile held as 32x32 MFMA accumulators:
+// wavefront (wm, wn) owns rows wm*WTM.. and columns wn*WTN.. as TM x TN
+// tiles; lane l holds columns 32j + 8q + 4(l/32) + r of row 32i + l%32.
+// Column-independent epilogues (store, GELU, residual) finish in registers
+// (bias, then GELU or the residual, one rounding to the output type, the
+// site statistics of the rounded values) and, when STAGE (the tile fits in
+// smem in the output type), leave through LDS with consecutive lanes on
+// consecutive columns: 16-byte chunks when output rows are 16-byte aligned,
+// single elements otherwise (the odd vocabulary of the head).  The gated and
+// rotary epilogues combine column groups 16 apart in registers (epi_pair).
+template <typename T, int BM, int BN, int WGM, int WGN, bool STAGE>
+__device__ __forceinline__ void tile_epilogue(const GemmArgs& a,
+                                              f32x16 (&acc)[BM / WGM / 32][BN / WGN / 32],
+                                              char* smem, int bm, int bn) {
+  constexpr int NT = 64 * WGM * WGN;
+  constexpr int WTM = BM / WGM, WTN = BN / WGN;
+  constexpr int TM = WTM / 32, TN = WTN / 32;
+  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
+  const int wm = wave / WGN, wn = wave % WGN;
+  const int l32 = lane & 31, g = lane >> 5;
+  __syncthreads();   // every wavefront is done reading operand tiles from smem
+  SiteMax sm;
+  if (STAGE && !a.kc && (a.epi == kEpiStore || a.epi == kEpiGelu || a.epi == kEpiResid)) {
+    // Column-independent epilogues finish in registers (bias, then GELU or
+    // the residual, one rounding to the output type, the site statistics
+    // of the rounded values) and stage the tile in LDS in the output type;
+    // rows then leave with consecutive lanes on consecutive columns: 16-byte
+    // chunks when output rows are 16-byte aligned, single elements otherwise
+    // (the odd vocabulary of the head).
+    constexpr int LDB = BN + 8;
+    T* stb = reinterpret_cast<T*>(smem);
+    const T* bias = static_cast<const T*>(a.bias);
+    const bool bias8 = (reinterpret_cast<uintptr_t>(bias) & 7) == 0;
+    T* out = static_cast<T*>(a.out);
+    const bool resid = a.epi == kEpiResid;
+    const T* res = static_cast<const T*>(a.resid);
+    const bool res8 = resid && (a.ldr & 3) == 0 && (reinterpret_cast<uintptr_t>(res) & 7) == 0;
+    static_for<0, TM>([&](auto i) {
+      const int ml = wm * WTM + 32 * i + l32;
+      const int m = bm + ml;
+      static_for<0, TN>([&](auto j) {
+        static_for<0, 4>([&](auto q) {
+          const int nl = wn * WTN + 32 * j + 8 * q + 4 * g;
+          const int n0 = bn + nl;
+          float v[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) v[r] = acc[i][j][4 * q + r];
+          if (bias) {
+            if (bias8 && n0 + 4 <= a.N) {
+              const u32x2 bb = *reinterpret_cast<const u32x2*>(bias + n0);
+              const T* be = reinterpret_cast<const T*>(&bb);
+#pragma unroll
+              for (int r = 0; r < 4; ++r) v[r] += to_f32(be[r]);
+            } else {
+#pragma unroll
+              for (int r = 0; r < 4; ++r)
+                if (n0 + r < a.N) v[r] += to_f32(bias[n0 + r]);
+            }
+          }
+          if (a.epi == kEpiGelu)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) v[r] = gelu_f(v[r]);
+          if (resid && m < a.M) {
+            const T* rrow = res + static_cast<long long>(m) * a.ldr + n0;
+            if (res8 && n0 + 4 <= a.N) {
+              const u32x2 rr = *reinterpret_cast<const u32x2*>(rrow);
+              const T* re = reinterpret_cast<const T*>(&rr);
+#pragma unroll
+              for (int r = 0; r < 4; ++r) v[r] += to_f32(re[r]);
+            } else {
+#pragma unroll
+              for (int r = 0; r < 4; ++r)
+                if (n0 + r < a.N) v[r] += to_f32(rrow[r]);
+            }
+          }
+          u32x2 w;
+          T* we = reinterpret_cast<T*>(&w);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) we[r] = from_f32<T>(v[r]);
+          if (resid && a.site >= 0 && m < a.M)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (n0 + r < a.N) sm.add(to_f32(we[r]));
+          *reinterpret_cast<u32x2*>(&stb[ml * LDB + nl]) = w;
+        });
+      });
+    });
+    __syncthreads();
+    if ((a.ldo & 7) == 0) {
+      constexpr int CPR = BN / 8;
+      const int ncol = a.N - bn < BN ? a.N - bn : BN;
+      for (int e = t; e < BM * CPR; e += NT) {
+        const int ml = e / CPR, j0 = 8 * (e % CPR);
+        const int m = bm + ml;
+        if (m >= a.M || j0 >= ncol) continue;
+        const u32x4 w = *reinterpret_cast<const u32x4*>(&stb[ml * LDB + j0]);
+        T* orow = out + static_cast<long long>(m) * a.ldo + bn;
+        if (j0 + 8 <= ncol) {
+          *reinterpret_cast<u32x4*>(orow + j0) = w;
+        } else {
+          const T* we = reinterpret_cast<const T*>(&w);
+#pragma unroll
+          for (int r = 0; r < 8; ++r)
+            if (j0 + r < ncol) orow[j0 + r] = we[r];
+        }
+      }
+    } else {
+      for (int e = t; e < BM * BN; e += NT) {
+        const int ml = e / BN, nl = e % BN;
+        const int m = bm + ml, n = bn + nl;
+        if (m >= a.M || n >= a.N) continue;
+        out[static_cast<long long>(m) * a.ldo + n] = stb[ml * LDB + nl];
+      }
+    }
+  } else {
+    static_for<0, TM>([&](auto i) {
+      const int m = bm + wm * WTM + 32 * i + l32;
+      static_for<0, TN>([&](auto j) {
+        static_for<0, 2>([&](auto q) {
+          const int nA = bn + wn * WTN + 32 * j + 8 * q + 4 * g;
+          float va[4], vb[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            va[r] = acc[i][j][4 * q + r];
+            vb[r] = acc[i][j][4 * (q + 2) + r];
+          }
+          epi_pair<T>(a, m, nA, va, vb, sm);
+        });
+      });
+    });
+  }
+  site_flush(a, sm);
+}
+
 template <typename T, int BM, int BN, int WGM, int WGN, int PF>
 __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm_x(GemmArgs a) {
   typedef typename Mfma32<T>::vec vec;
@@ -373,117 +507,195 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm_x(GemmArgs a) {
     });
   }
 
-  SiteMax sm;
-  if (STAGE && !a.kc && (a.epi == kEpiStore || a.epi == kEpiGelu || a.epi == kEpiResid)) {
-    // Column-independent epilogues finish in registers (bias, then GELU or
-    // the residual, one rounding to the output type, the site statistics
-    // of the rounded values) and stage the tile in LDS in the output type;
-    // rows then leave with consecutive lanes on consecutive columns: 16-byte
-    // chunks when output rows are 16-byte aligned, single elements otherwise
-    // (the odd vocabulary of the head).
-    constexpr int LDB = BN + 8;
-    T* stb = reinterpret_cast<T*>(smem);
-    const T* bias = static_cast<const T*>(a.bias);
-    const bool bias8 = (reinterpret_cast<uintptr_t>(bias) & 7) == 0;
-    T* out = static_cast<T*>(a.out);
-    const bool resid = a.epi == kEpiResid;
-    const T* res = static_cast<const T*>(a.resid);
-    const bool res8 = resid && (a.ldr & 3) == 0 && (reinterpret_cast<uintptr_t>(res) & 7) == 0;
-    static_for<0, TM>([&](auto i) {
-      const int ml = wm * WTM + 32 * i + l32;
-      const int m = bm + ml;
-      static_for<0, TN>([&](auto j) {
-        static_for<0, 4>([&](auto q) {
-          const int nl = wn * WTN + 32 * j + 8 * q + 4 * g;
-          const int n0 = bn + nl;
-          float v[4];
+  tile_epilogue<T, BM, BN, WGM, WGN, STAGE>(a, acc, smem, bm, bn);
+}
+
+// ------------------------------------------------------------ large-tile kernel
+// For products with enough tiles of 256 x 256 (or 256 x 128): 8 wavefronts
+// of 128 x 64 (WGM x WGN = 2 x 4) on v_mfma_f32_32x32x16, the same operand
+// roles, k order and epilogue as k_gemm_x, so the results are the same bits.
+// A wavefront tile of 128 x 64 reads 6 KB of LDS per 8 MFMAs (the 64 x 32
+// tile of k_gemm_x reads 3 KB per 2), and a 256 x 256 workgroup tile loads
+// half the bytes per flop from L2 of a 128 x 128 one.
+// Operand tiles travel from global memory straight into LDS
+// (global_load_lds_dwordx4: lane i of a wavefront instruction writes bytes
+// 16i..16i+15 of a 1 KB block), through a ring of NS stages of BK columns.
+// A row of BK bf16 is CPR 16-byte chunks; chunk c of row r is stored in slot
+// c ^ ((r / RPB) % CPR), RPB = rows per 256 bytes, so the 16 rows that 16
+// consecutive lanes read at once (one MFMA operand fragment) fall into 16
+// distinct 16-byte bank groups of the 64 four-byte banks.
+// Loop schedule: the fragments of the next k-step are read while the MFMAs
+// of the current one run, and across stages too: before the last k-step of
+// stage k the wavefront waits for its loads of stage k+1, meets the others
+// at the barrier (after it nobody reads stage k any more, and stage k+1 is
+// in LDS), issues the loads of stage k+NS into stage k's slot and the
+// fragment reads of stage k+1, then runs the MFMAs of stage k's last k-step.
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+__device__ __forceinline__ void dma16(const void* g, void* lds) {
+  __builtin_amdgcn_global_load_lds(g, (lds_ptr_t)lds, 16, 0, 0);
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+__device__ __forceinline__ void wait_lgkmcnt0() {
+  __builtin_amdgcn_s_waitcnt(0xF | (0x3 << 14) | (0x7 << 4));   // lgkmcnt(0), others untouched
+}
+
+template <typename T, int BM, int BN, int WGM, int WGN, int BK, int NS>
+__global__ __launch_bounds__(64 * WGM * WGN)
+__attribute__((amdgpu_waves_per_eu(WGM * WGN / 4, WGM * WGN / 4))) void k_gemm_big(GemmArgs a) {
+  typedef typename Mfma32<T>::vec vec;
+  constexpr int NW = WGM * WGN;
+  constexpr int WTM = BM / WGM, WTN = BN / WGN;
+  constexpr int TM = WTM / 32, TN = WTN / 32;
+  constexpr int KS = BK / 16;                           // k-steps per stage
+  constexpr int CPR = BK * 2 / 16;                      // 16-byte chunks per row
+  constexpr int RPB = 16 / CPR;                         // rows per 256 bytes
+  constexpr int RPI = 1024 / (BK * 2);                  // rows per wavefront instruction
+  constexpr int STAGE_ELEMS = (BM + BN) * BK;
+  constexpr int LPW = (BM + BN) / RPI / NW;             // loads per wavefront per stage
+  constexpr int RING = NS * STAGE_ELEMS * 2;
+  constexpr int OUTB = BM * (BN + 8) * 2;
+  constexpr int SMEM = RING > OUTB ? RING : OUTB;
+  static_assert(sizeof(T) == 2, "16-bit operands");
+  static_assert((BM + BN) % (RPI * NW) == 0, "stage rows must split over the wavefronts");
+  static_assert(LPW * (NS - 1) < 64, "vmcnt range");
+  static_assert(KS % 2 == 0, "fragment sets alternate per k-step across stages");
+  __shared__ __attribute__((aligned(1024))) char smem[SMEM];
+  T* lds = reinterpret_cast<T*>(smem);
+  const int tiles_m = (a.M + BM - 1) / BM, tiles_n = (a.N + BN - 1) / BN;
+  int tm, tn;
+  tile_of(blockIdx.x, tiles_m, tiles_n, tm, tn);
+  const int bm = tm * BM, bn = tn * BN;
+  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
+  const T* __restrict__ A0 = static_cast<const T*>(a.A);
+  const T* __restrict__ W0 = static_cast<const T*>(a.W);
+
+  // this lane's source for each of its LPW loads: stage row
+  // sr = (wave * LPW + j) * RPI + lane / CPR (rows < BM: activations, the
+  // rest weight rows), chunk chosen so that it lands in its swizzled slot
+  const T* src[LPW];
 #pragma unroll
-          for (int r = 0; r < 4; ++r) v[r] = acc[i][j][4 * q + r];
-          if (bias) {
-            if (bias8 && n0 + 4 <= a.N) {
-              const u32x2 bb = *reinterpret_cast<const u32x2*>(bias + n0);
-              const T* be = reinterpret_cast<const T*>(&bb);
-#pragma unroll
-              for (int r = 0; r < 4; ++r) v[r] += to_f32(be[r]);
-            } else {
-#pragma unroll
-              for (int r = 0; r < 4; ++r)
-                if (n0 + r < a.N) v[r] += to_f32(bias[n0 + r]);
-            }
-          }
-          if (a.epi == kEpiGelu)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) v[r] = gelu_f(v[r]);
-          if (resid && m < a.M) {
-            const T* rrow = res + static_cast<long long>(m) * a.ldr + n0;
-            if (res8 && n0 + 4 <= a.N) {
-              const u32x2 rr = *reinterpret_cast<const u32x2*>(rrow);
-              const T* re = reinterpret_cast<const T*>(&rr);
-#pragma unroll
-              for (int r = 0; r < 4; ++r) v[r] += to_f32(re[r]);
-            } else {
-#pragma unroll
-              for (int r = 0; r < 4; ++r)
-                if (n0 + r < a.N) v[r] += to_f32(rrow[r]);
-            }
-          }
-          u32x2 w;
-          T* we = reinterpret_cast<T*>(&w);
-#pragma unroll
-          for (int r = 0; r < 4; ++r) we[r] = from_f32<T>(v[r]);
-          if (resid && a.site >= 0 && m < a.M)
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-              if (n0 + r < a.N) sm.add(to_f32(we[r]));
-          *reinterpret_cast<u32x2*>(&stb[ml * LDB + nl]) = w;
-        });
-      });
-    });
-    __syncthreads();
-    if ((a.ldo & 7) == 0) {
-      constexpr int CPR = BN / 8;
-      const int ncol = a.N - bn < BN ? a.N - bn : BN;
-      for (int e = t; e < BM * CPR; e += NT) {
-        const int ml = e / CPR, j0 = 8 * (e % CPR);
-        const int m = bm + ml;
-        if (m >= a.M || j0 >= ncol) continue;
-        const u32x4 w = *reinterpret_cast<const u32x4*>(&stb[ml * LDB + j0]);
-        T* orow = out + static_cast<long long>(m) * a.ldo + bn;
-        if (j0 + 8 <= ncol) {
-          *reinterpret_cast<u32x4*>(orow + j0) = w;
-        } else {
-          const T* we = reinterpret_cast<const T*>(&w);
-#pragma unroll
-          for (int r = 0; r < 8; ++r)
-            if (j0 + r < ncol) orow[j0 + r] = we[r];
-        }
-      }
+  for (int j = 0; j < LPW; ++j) {
+    const int sr = (wave * LPW + j) * RPI + lane / CPR;
+    const int chunk = (lane % CPR) ^ ((sr / RPB) % CPR);
+    if (sr < BM) {
+      int r = bm + sr;
+      r = r < a.M ? r : a.M - 1;
+      src[j] = A0 + static_cast<long long>(r) * a.lda + chunk * 8;
     } else {
-      for (int e = t; e < BM * BN; e += NT) {
-        const int ml = e / BN, nl = e % BN;
-        const int m = bm + ml, n = bn + nl;
-        if (m >= a.M || n >= a.N) continue;
-        out[static_cast<long long>(m) * a.ldo + n] = stb[ml * LDB + nl];
-      }
+      int c = bn + sr - BM;
+      c = c < a.N ? c : a.N - 1;
+      src[j] = W0 + static_cast<long long>(c) * a.ldw + chunk * 8;
     }
-  } else {
-    static_for<0, TM>([&](auto i) {
-      const int m = bm + wm * WTM + 32 * i + l32;
-      static_for<0, TN>([&](auto j) {
-        static_for<0, 2>([&](auto q) {
-          const int nA = bn + wn * WTN + 32 * j + 8 * q + 4 * g;
-          float va[4], vb[4];
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            va[r] = acc[i][j][4 * q + r];
-            vb[r] = acc[i][j][4 * (q + 2) + r];
-          }
-          epi_pair<T>(a, m, nA, va, vb, sm);
-        });
-      });
-    });
   }
-  site_flush(a, sm);
+  auto issue = [&](int buf, int k0) {
+#pragma unroll
+    for (int j = 0; j < LPW; ++j)
+      dma16(src[j] + k0, lds + buf * STAGE_ELEMS + (wave * LPW + j) * RPI * BK);
+  };
+
+  const int wm = wave / WGN, wn = wave % WGN;
+  const int l32 = lane & 31, g = lane >> 5;
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  // fragment rows differ by multiples of 32 from l32, so the swizzle term
+  // depends on the lane only
+  const int swz = (l32 / RPB) % CPR;
+  const int offA = (wm * WTM + l32) * BK, offB = (BM + wn * WTN + l32) * BK;
+  vec fa[2][TM], fb[2][TN];
+  auto read_frags = [&](auto set, int buf, int ks) {
+    const T* st = lds + buf * STAGE_ELEMS;
+    const int col = ((2 * ks + g) ^ swz) * 8;
+#pragma unroll
+    for (int j = 0; j < TN; ++j) fb[set][j] = *reinterpret_cast<const vec*>(st + offB + 32 * j * BK + col);
+#pragma unroll
+    for (int i = 0; i < TM; ++i) fa[set][i] = *reinterpret_cast<const vec*>(st + offA + 32 * i * BK + col);
+  };
+  auto mfmas = [&](auto set) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) acc[i][j] = Mfma32<T>::run(fb[set][j], fa[set][i], acc[i][j]);
+  };
+
+  const int nk = a.K / BK;
+  // every slot of the ring starts loading
+  static_for<0, NS>([&](auto st) {
+    if (st < nk) issue(st, st * BK);
+  });
+  // stage 0 landed (the younger NS - 1 stages may stay in flight)
+  if (nk >= NS) wait_vmcnt<LPW * (NS - 1)>();
+  else wait_vmcnt<0>();
+  __builtin_amdgcn_s_barrier();
+  read_frags(std::integral_constant<int, 0>{}, 0, 0);
+  // One stage.  STEADY: stage k + NS exists, so NS - 2 younger stages stay
+  // in flight at the wait and the loads of stage k + NS are issued; the
+  // steady loop has no branches, so the compiler's waits before the MFMAs
+  // of the last k-step only cover fragments read before the barrier.
+  auto stage = [&](auto steady, int k) {
+    const int buf = k % NS;
+    static_for<0, KS>([&](auto KSI) {
+      constexpr int ks = decltype(KSI)::value;
+      constexpr int cur = ks & 1;   // KS is even: the set of (k, ks) is ks & 1
+      constexpr int NF = TM + TN, NM = TM * TN;   // fragment reads, MFMAs per k-step
+      if constexpr (ks + 1 < KS) {
+        read_frags(std::integral_constant<int, cur ^ 1>{}, buf, ks + 1);
+        mfmas(std::integral_constant<int, cur>{});
+        // one MFMA, then one fragment read, alternating
+        static_for<0, NM>([&](auto q) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          if constexpr (decltype(q)::value < NF) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        });
+      } else if constexpr (decltype(steady)::value) {
+        wait_vmcnt<LPW * (NS - 2)>();   // stage k+1 landed
+        wait_lgkmcnt0();                // this wavefront's reads of stage k are complete
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        issue(buf, (k + NS) * BK);
+        read_frags(std::integral_constant<int, cur ^ 1>{}, (k + 1) % NS, 0);
+        mfmas(std::integral_constant<int, cur>{});
+        // the loads of stage k+NS, then the fragment reads of stage k+1,
+        // each between two MFMAs
+        static_for<0, NM>([&](auto q) {
+          constexpr int i = decltype(q)::value;
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          if constexpr (i < LPW) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+          else if constexpr (i - LPW < NF) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        });
+      } else {
+        if (k + 1 < nk) {
+          wait_vmcnt<0>();
+          wait_lgkmcnt0();
+          __builtin_amdgcn_s_barrier();
+          asm volatile("" ::: "memory");
+          read_frags(std::integral_constant<int, cur ^ 1>{}, (k + 1) % NS, 0);
+        }
+        mfmas(std::integral_constant<int, cur>{});
+      }
+    });
+  };
+  int k = 0;
+  for (; k + NS < nk; ++k) stage(std::true_type{}, k);
+  for (; k < nk; ++k) stage(std::false_type{}, k);
+  tile_epilogue<T, BM, BN, WGM, WGN, (OUTB <= SMEM)>(a, acc, smem, bm, bn);
+}
+
+template <typename T, int BM, int BN, int WGM, int WGN, int BK, int NS>
+static void run_big(const GemmArgs& a, hipStream_t s) {
+  const dim3 grid(((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN));
+  hipLaunchKernelGGL((k_gemm_big<T, BM, BN, WGM, WGN, BK, NS>), grid, dim3(64 * WGM * WGN), 0, s, a);
 }
 
 template <typename T, int BM, int BN, int WGM, int WGN, int PF>
@@ -494,13 +706,25 @@ static void run_x(const GemmArgs& a, hipStream_t s) {
 
 template <typename T>
 static void gemm_mfma(const GemmArgs& a, hipStream_t s) {
-  // 128 x 128 workgroup tiles, 8 wavefronts of 64 x 32, operands fetched two
-  // K steps ahead (the best of the measured configurations on the projection
-  // and head shapes).  Products too small to give the chip ~160 such tiles
-  // (1024-row decoder GEMMs of an encoder-decoder: N 768 gives 48) take
-  // 64 x 64 tiles on 4 wavefronts of 32 x 32: four times the workgroups.
-  const long long tiles128 = ((a.M + 127) / 128) * static_cast<long long>((a.N + 127) / 128);
-  if (tiles128 < 160) run_x<T, 64, 64, 2, 2, 2>(a, s);
+  // Long products (K >= 2048: the 4096-wide decoder's projections and head)
+  // take the large-tile kernel, with the tile that fills the chip best:
+  // 256 x 256 when there are two or more waves of such tiles (256 CUs), a
+  // K step of 64 in two stages at 1.25 - 2 waves, 256 x 128 from one wave
+  // on (O and down at 2048 x 4096).  Measured on those shapes, same bits.
+  // Shorter K (the 768- and 1024-wide models) stays on 128 x 128 tiles, 8
+  // wavefronts of 64 x 32, operands fetched two K steps ahead; products too
+  // small to give the chip ~160 such tiles (1024-row decoder GEMMs of an
+  // encoder-decoder: N 768 gives 48) take 64 x 64 tiles on 4 wavefronts of
+  // 32 x 32: four times the workgroups.
+  auto tiles = [&](int bm, int bn) {
+    return ((a.M + bm - 1) / bm) * static_cast<long long>((a.N + bn - 1) / bn);
+  };
+  if (a.K >= 2048) {
+    if (tiles(256, 256) >= 512) return run_big<T, 256, 256, 2, 4, 32, 4>(a, s);
+    if (tiles(256, 256) >= 320) return run_big<T, 256, 256, 2, 4, 64, 2>(a, s);
+    if (tiles(256, 128) >= 224) return run_big<T, 256, 128, 2, 4, 64, 3>(a, s);
+  }
+  if (tiles(128, 128) < 160) run_x<T, 64, 64, 2, 2, 2>(a, s);
   else run_x<T, 128, 128, 2, 4, 2>(a, s);
 }
 

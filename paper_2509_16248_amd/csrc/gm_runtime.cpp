@@ -306,6 +306,30 @@ struct Prof {
   }
 };
 
+// Activation workspace of one forward (h, a, qkv, ctx, f and, post-norm,
+// tmp): the model's own buffers unless a caller supplies others.
+struct Work {
+  void *h = nullptr, *a = nullptr, *qkv = nullptr, *ctx = nullptr, *f = nullptr, *tmp = nullptr;
+};
+
+// Storage points of every layer, copied during a debug forward
+// (gm_debug_forward_layers) into one caller buffer: per layer, in elements
+// of the activation dtype, a1 [T, d] | qkv [T, 3d] | ctx [T, d] |
+// h_mid [T, d] | a2 [T, d] | f [T, ff] | h_out [T, d].
+struct Dump {
+  char* base = nullptr;
+  size_t esz = 0;
+  size_t T = 0, d = 0, ff = 0;
+  size_t layer_elems() const { return T * (8 * d + ff); }
+  void copy(int layer, int which, const void* src, hipStream_t s) const {
+    static const int kStart[7] = {0, 1, 4, 5, 6, 7, -1};   // in units of T*d (h_out after f)
+    const size_t width = which == 1 ? 3 * d : which == 5 ? ff : d;
+    const size_t off = which == 6 ? T * (7 * d + ff) : static_cast<size_t>(kStart[which]) * T * d;
+    (void)hipMemcpyAsync(base + (layer * layer_elems() + off) * esz, src, T * width * esz,
+                         hipMemcpyDeviceToDevice, s);
+  }
+};
+
 // Segment selection for the fragmented (unmended) execution: the forward is
 // cut at every point where the original program reads a device value back
 // on the host; only the launches of segment `want` are issued (want < 0:
@@ -323,8 +347,16 @@ constexpr int kCountOnly = -2;
 // sequence at position seqlen[b], attending to the cache).
 void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
              void* logits, hipStream_t s, Prof* prof = nullptr, Seg* seg = nullptr,
-             const Dec* dec = nullptr) {
+             const Dec* dec = nullptr, const Dump* dump = nullptr, const Work* work = nullptr) {
   const gm_config& c = m->cfg;
+  Work own;
+  own.h = m->h;
+  own.a = m->a;
+  own.qkv = m->qkv;
+  own.ctx = m->ctx;
+  own.f = m->f;
+  own.tmp = m->tmp;
+  const Work& wk = work ? *work : own;
   auto on = [&]() { return !seg || seg->want == -1 || seg->want == seg->cur; };
   auto brk = [&](int kind) {
     if (seg) {
@@ -373,11 +405,11 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
   r.seq = S;
   r.pos = dec ? m->dpos : nullptr;
   r.vocab = c.vocab;
-  r.x = m->h;
+  r.x = wk.h;
   r.norm = c.emb_norm ? normk : -1;
   r.g = m->emb_ln_g;
   r.b = m->emb_ln_b;
-  r.out = m->h;
+  r.out = wk.h;
   r.clamp_site = -1;
   if (on()) launch_rownorm(r, s);
   P(GM_K_EMBED, -1, 0.0, static_cast<double>(T) * d * es * (c.pos == GM_POS_LEARNED ? 3 : 2));
@@ -390,12 +422,12 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
   auto layers_and_head = [&](hipStream_t s, int b0, int nb) {
   const int T = nb * S;
   const size_t ro = static_cast<size_t>(b0) * S;   // first row of this part
-  char* hh = static_cast<char*>(m->h) + ro * d * m->esz;
-  char* aa = static_cast<char*>(m->a) + ro * d * m->esz;
-  char* qq = static_cast<char*>(m->qkv) + ro * 3 * d * m->esz;
-  char* cc = static_cast<char*>(m->ctx) + ro * d * m->esz;
-  char* ffb = static_cast<char*>(m->f) + ro * ff * m->esz;
-  char* tt = m->tmp ? static_cast<char*>(m->tmp) + ro * d * m->esz : nullptr;
+  char* hh = static_cast<char*>(wk.h) + ro * d * m->esz;
+  char* aa = static_cast<char*>(wk.a) + ro * d * m->esz;
+  char* qq = static_cast<char*>(wk.qkv) + ro * 3 * d * m->esz;
+  char* cc = static_cast<char*>(wk.ctx) + ro * d * m->esz;
+  char* ffb = static_cast<char*>(wk.f) + ro * ff * m->esz;
+  char* tt = wk.tmp ? static_cast<char*>(wk.tmp) + ro * d * m->esz : nullptr;
   char* lg = static_cast<char*>(logits) + ro * c.vocab * m->esz;
   auto norm_rows = [&](void* x, void* out, const void* g, const void* b, int site) {
     RowArgs q = r;
@@ -551,13 +583,23 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
     const LayerBufs& L = m->layers[l];
     const int s0 = ns ? 2 * l : -1, s1 = ns ? 2 * l + 1 : -1;
     if (pre) {
+      auto D = [&](int which, const void* src) {
+        if (dump) dump->copy(l, which, src, s);
+      };
       norm_rows(hh, aa, L.ln1_g, L.ln1_b, prev_site);
+      D(0, aa);
       gemm(GM_K_GEMM_QKV, aa, d, L.wqkv, 3 * d, qkv_epi, L.bqkv, qq, 3 * d, nullptr, -1);
+      D(1, qq);
       attention();
+      D(2, cc);
       gemm(GM_K_GEMM_O, cc, d, L.wo, d, kEpiResid, L.bo, hh, d, hh, s0);
+      D(3, hh);
       norm_rows(hh, aa, L.ln2_g, L.ln2_b, s0);
+      D(4, aa);
       gemm(GM_K_GEMM_UP, aa, d, L.w1, up_n, up_epi, L.b1, ffb, ff, nullptr, -1);
+      D(5, ffb);
       gemm(GM_K_GEMM_DOWN, ffb, ff, L.w2, d, kEpiResid, L.b2, hh, d, hh, s1);
+      D(6, hh);
       prev_site = s1;
     } else {
       gemm(GM_K_GEMM_QKV, hh, d, L.wqkv, 3 * d, qkv_epi, L.bqkv, qq, 3 * d, nullptr, -1);
@@ -600,7 +642,7 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
   int parts = m->split_parts < B ? m->split_parts : B;
   // (a decode step's parts run the skinny kernels, so any part size goes)
   while (!dec && parts > 1 && (B / parts) * S <= 16) --parts;
-  if (prof || c.fp16_clamp || c.log_hidden || (c.kv_cache && !dec)) parts = 1;
+  if (prof || dump || work || c.fp16_clamp || c.log_hidden || (c.kv_cache && !dec)) parts = 1;
   head_joined = parts > 1 && dec;
   if (parts > 1) {
     // (the graph-broken run splits the same way: its only cut, the guards,
@@ -625,7 +667,7 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
       q.M = B;
       q.N = c.vocab;
       q.K = d;
-      q.A = pre ? m->a : m->h;   // the final norm's output, or the stream itself
+      q.A = pre ? wk.a : wk.h;   // the final norm's output, or the stream itself
       q.lda = d;
       q.W = m->head;
       q.ldw = d;
@@ -1472,6 +1514,33 @@ int gm_profile_forward(gm_model* m, int32_t B, int32_t S, const int32_t* ids,
   }
   for (hipEvent_t ev : prof.ev) hipEventDestroy(ev);
   return rc;
+}
+
+int gm_debug_forward_layers(gm_model* m, int32_t B, int32_t S, const int32_t* ids,
+                            const int32_t* mask, void* logits, hipStream_t stream, void* dump,
+                            uint64_t dump_bytes) {
+  if (!m || !dump) return inval("NULL argument");
+  const gm_config& c = m->cfg;
+  if (c.n_dec_layers || c.norm_place != GM_NORM_PRE)
+    return inval("layer dumps cover pre-norm decoder-only and encoder-only models");
+  if (!ids || !mask || !logits) return inval("ids, mask and logits must be non-NULL");
+  if ((reinterpret_cast<uintptr_t>(ids) | reinterpret_cast<uintptr_t>(mask) |
+       reinterpret_cast<uintptr_t>(logits) | reinterpret_cast<uintptr_t>(dump)) & 15)
+    return inval("ids, mask, logits and dump must be 16-byte aligned");
+  if (B < 1 || B > c.max_batch || S < 1 || S > c.max_seq) return inval("B or S out of range");
+  Dump d;
+  d.base = static_cast<char*>(dump);
+  d.esz = m->esz;
+  d.T = static_cast<size_t>(B) * S;
+  d.d = c.d_model;
+  d.ff = c.d_ff;
+  if (dump_bytes < c.n_layers * d.layer_elems() * d.esz) return inval("dump buffer too small");
+  m->stats.forwards++;
+  m->stats.eager_forwards++;
+  if (c.kv_cache) m->cache_B = B;
+  enqueue(m, B, S, ids, mask, logits, stream, nullptr, nullptr, nullptr, &d);
+  HIP_TRY(hipGetLastError());
+  return GM_OK;
 }
 
 int gm_forward(gm_model* m, const int32_t* ids, const int32_t* mask, void* logits,

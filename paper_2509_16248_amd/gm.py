@@ -103,7 +103,8 @@ gm_effect_cb = ctypes.CFUNCTYPE(None, ctypes.POINTER(gm_effect), ctypes.c_void_p
 EXPORTS = ["gm_model_create", "gm_model_destroy", "gm_forward", "gm_forward_ex",
            "gm_decode_step", "gm_set_mask_guard", "gm_trap_info", "gm_forward_seq2seq",
            "gm_profile_forward", "gm_set_exec_mode", "gm_set_graph_mode", "gm_read_decisions", "gm_decisions_device_ptr",
-           "gm_check_error", "gm_flush_effects", "gm_debug_buffer", "gm_get_stats",
+           "gm_check_error", "gm_flush_effects", "gm_debug_buffer", "gm_debug_forward_layers",
+           "gm_get_stats",
            "gm_strerror",
            "gm_last_error"]
 
@@ -139,6 +140,7 @@ def lib(path: str = LIB_PATH) -> ctypes.CDLL:
     L.gm_check_error.argtypes = [_vp, ctypes.POINTER(_i32), ctypes.POINTER(_i32)]
     L.gm_flush_effects.argtypes = [_vp, gm_effect_cb, _vp, ctypes.POINTER(_i32)]
     L.gm_debug_buffer.argtypes = [_vp, _i32, ctypes.POINTER(_vp), ctypes.POINTER(_u64)]
+    L.gm_debug_forward_layers.argtypes = [_vp, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _u64]
     L.gm_get_stats.argtypes = [_vp, ctypes.POINTER(gm_stats)]
     L.gm_strerror.argtypes = [ctypes.c_int]
     L.gm_strerror.restype = ctypes.c_char_p
@@ -283,6 +285,12 @@ def gm_debug_buffer(m: int, which: int):
     p, n = _vp(), _u64()
     _check(lib().gm_debug_buffer(m, which, ctypes.byref(p), ctypes.byref(n)), "gm_debug_buffer")
     return p.value, n.value
+
+
+def gm_debug_forward_layers(m: int, B: int, S: int, ids: int, mask: int, logits: int,
+                            stream: int, dump: int, dump_bytes: int) -> None:
+    _check(lib().gm_debug_forward_layers(m, B, S, ids, mask, logits, stream, dump, dump_bytes),
+           "gm_debug_forward_layers")
 
 
 def gm_get_stats(m: int) -> gm_stats:

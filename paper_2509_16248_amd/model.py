@@ -232,6 +232,26 @@ class GmModel:
         assert rc == 0, rc
         return out
 
+    def forward_layers(self, ids: torch.Tensor, mask: torch.Tensor, logits: torch.Tensor,
+                       stream=None) -> dict:
+        """Forward (gm_debug_forward_layers) that also returns every layer's
+        storage points as device tensors: name -> [n_layers, T, width] with
+        names a1, qkv, ctx, h_mid, a2, f, h_out (T = B * S)."""
+        B, S = ids.shape
+        T, d, ff, L = B * S, self.c.d_model, self.c.d_ff, self.c.n_layers
+        widths = [("a1", d), ("qkv", 3 * d), ("ctx", d), ("h_mid", d), ("a2", d), ("f", ff),
+                  ("h_out", d)]
+        per = T * (8 * d + ff)
+        dump = torch.empty((L, per), dtype=_TORCH[self.cfg.dtype], device=self.device)
+        gm.gm_debug_forward_layers(self.handle, B, S, ids.data_ptr(), mask.data_ptr(),
+                                   logits.data_ptr(), self._stream(stream), dump.data_ptr(),
+                                   dump.numel() * dump.element_size())
+        out, off = {}, 0
+        for name, wdt in widths:
+            out[name] = dump[:, off:off + T * wdt].view(L, T, wdt)
+            off += T * wdt
+        return out
+
     def stats(self) -> dict:
         s = gm.gm_get_stats(self.handle)
         return {k: getattr(s, k) for k, _ in gm.gm_stats._fields_}

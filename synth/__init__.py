@@ -19,8 +19,8 @@ for them:
                         (0..256 trailing pads per sequence)
 * ``encoder_clamp_1024`` 24 layers, d=1024, 16 heads, gated-GELU FFN 2816,
                         RMSNorm, fp16, batch 4 x seq 1024, weights N(0,0.05)
-                        with 1% of matrix entries scaled x200 (overflow guard;
-                        not in the query/key projection rows)
+                        with 1% of the entries of every matrix scaled x200
+                        (overflow guard)
 * ``decoder_4096``      32 layers, d=4096, 32 heads, SwiGLU FFN 11008,
                         RMSNorm, rotary (base 1e4, cache 1024 grown on
                         demand), vocab 32000, batch 1 x seq 2048, bf16
@@ -310,12 +310,6 @@ def _draw(cfg: ModelConfig, seed: int, name: str, layer: Optional[int],
         x += np.float32(1.0)
     elif name in MATRICES and cfg.outlier_frac > 0:
         sel = rng.random(shape, dtype=np.float32) < cfg.outlier_frac
-        if name == "wqkv":
-            # q and k rows keep plain N(0, sigma) weights: outliers there only
-            # sharpen attention into a near-argmax whose winner a one-ulp
-            # rounding difference can flip; they play no part in making the
-            # residual stream overflow.
-            sel[:2 * cfg.d_model] = False
         x[sel] *= np.float32(cfg.outlier_scale)
     return encode(x, cfg.dtype)
 

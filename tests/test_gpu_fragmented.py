@@ -2,7 +2,10 @@
 per region between graph breaks, with a host synchronisation, a read-back
 and a host-side branch at every break.  It launches the same kernels, so
 its results must equal the single-graph forward bit for bit, while its
-counters show the breaks the single-graph forward removes."""
+counters show the breaks the single-graph forward removes.  Each graph-broken
+run is also compared with the oracle on the same inputs: the decisions its
+host branches took (padding, rotary regrow, every clamp site) exactly, the
+logits within the parity tolerance."""
 import numpy as np
 import pytest
 import torch
@@ -10,7 +13,7 @@ import torch
 import synth
 from oracle import TRAP_TOKEN_RANGE, OracleModel
 
-from test_gpu_parity import gpu_effects, gpu_model
+from test_gpu_parity import check_decisions, check_logits, f64, gpu_effects, gpu_model
 
 pytestmark = pytest.mark.gpu
 
@@ -35,6 +38,7 @@ def test_fragmented_equals_single_graph(name, n_breaks):
     out_a = a.new_logits(*ids.shape)
     out_b = b.new_logits(*ids.shape)
     b.set_exec_mode("fragmented")
+    orc = OracleModel(cfg, w)
     for k in range(2):     # the rotary model regrows in the first call only
         ra = _forward(a, ids_t, mask_t, out_a)
         s0 = b.stats()
@@ -42,6 +46,9 @@ def test_fragmented_equals_single_graph(name, n_breaks):
         s1 = b.stats()
         assert torch.equal(ra.view(torch.int16), rb.view(torch.int16)), f"call {k}"
         assert a.decisions() == b.decisions()
+        res = orc.forward(ids, mask)
+        check_decisions(b.decisions(), res, cfg)
+        check_logits(f64(rb), res.logits_f64, cfg.dtype, f"{name} graph-broken call {k}")
         assert s1["host_syncs_in_forward"] - s0["host_syncs_in_forward"] == n_breaks
         assert s1["graph_launches"] - s0["graph_launches"] == n_breaks + 1
         print(f"{name} call {k}: {n_breaks} breaks, {n_breaks + 1} graphs", flush=True)

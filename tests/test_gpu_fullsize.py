@@ -3,22 +3,31 @@
 Each model runs at its full shape in one graph launch (as in the benchmark);
 the oracle recomputes what it can afford on the host: whole sequences of an
 encoder (sequences are independent apart from the batch-wide padding
-predicate, which the oracle still takes over the whole batch), a causal
-prefix of the long decoder (with a causal mask a prefix does not depend on
-later positions), and the whole batch of the fp16 clamp model (its clamp
-predicate reads every sequence).
+predicate, which the oracle still takes over the whole batch), all 2048
+positions of the long decoder at 2 layers and a causal prefix at 32 (with a
+causal mask a prefix does not depend on later positions), and the whole batch
+of the fp16 clamp model (its clamp predicate reads every sequence).  Every
+step of every layer of the two deep models is compared at 2e-2 in
+test_gpu_stepwise.py.
 
 Depth and tolerance.  Two of the workloads amplify rounding-level
-differences with depth: evaluating the oracle's own definition with float32
-instead of float64 accumulation moves its logits by 0.38 (relative to the
-largest logit) on the 24-layer fp16 clamp model (differences grow about
-1.3x per layer) and by 0.0435 on the 32-layer rotary decoder.  No
-implementation whose summation order differs from the oracle's can meet
-2e-2 there.  So each is checked (a) at full width, batch and sequence with
-the depth cut to where the same spread is below 2e-2 (8 layers: 0.0066; 2
-layers), against 2e-2, and (b) at full depth with every decision and effect
-exact and the logits within twice the measured spread.
+differences with depth.  tests/golden/depth_spread.py measures how far the
+oracle's own program moves when it is evaluated with float32 instead of
+float64 arithmetic (relative to the largest logit): for the fp16 clamp
+model 0.0076 at 2 layers, 0.0165 at 4, 0.056 at 8 and 1.04 at 24 (its q/k
+outliers make attention a near-argmax, the overflowing residual stream is
+clamped at every site after the first); for the 32-layer rotary decoder the
+value stored in depth_spread.json.  No implementation whose summation order
+differs from the oracle's can be held closer than that.  So the logits are
+compared at 2e-2 where the spread is below 1e-2 (2 layers), within twice the
+spread where it is larger but informative (8 layers, the 32-layer decoder),
+and not at all where it is about 1 (the 24-layer clamp model: its decisions
+and effects are still compared exactly, and test_gpu_stepwise.py checks every
+step of every layer).
 """
+import json
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -31,8 +40,9 @@ from test_gpu_parity import (check_decisions, check_logits, effects_of, f64,
 
 pytestmark = pytest.mark.gpu
 
-# twice the float32-vs-float64 spread of the oracle itself at full depth
-FULL_DEPTH_TOL = {"encoder_clamp_1024": 2 * 0.38, "decoder_4096": 2 * 0.0435}
+# the float32-vs-float64 spread of the oracle's own program (depth_spread.py)
+SPREAD = json.load(open(os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                                     "depth_spread.json")))
 
 
 def test_full_encoder_1024_sampled_sequences():
@@ -65,15 +75,24 @@ def _clamp_case(cfg, wseed, tol):
     out = run(m, ids, mask)
     check_decisions(m.decisions(), res, cfg)
     assert gpu_effects(m) == effects_of(res)
-    check_logits(f64(out), res.logits_f64, cfg.dtype, f"{cfg.name} {cfg.n_layers} layers", tol)
+    if tol is not False:
+        check_logits(f64(out), res.logits_f64, cfg.dtype, f"{cfg.name} {cfg.n_layers} layers", tol)
+
+
+def test_encoder_clamp_1024_full_width_2_layers():
+    _clamp_case(synth.preset("encoder_clamp_1024", n_layers=2), 5, None)
 
 
 def test_encoder_clamp_1024_full_width_8_layers():
-    _clamp_case(synth.preset("encoder_clamp_1024", n_layers=8), 5, None)
+    _clamp_case(synth.preset("encoder_clamp_1024", n_layers=8), 5,
+                2 * SPREAD["encoder_clamp_1024"]["8"])
 
 
 def test_encoder_clamp_1024_full_depth():
-    _clamp_case(synth.preset("encoder_clamp_1024"), 5, FULL_DEPTH_TOL["encoder_clamp_1024"])
+    """Decisions of all 48 sites and the effect records, exactly; the logits
+    carry no information at this depth (spread about 1, see above)."""
+    assert SPREAD["encoder_clamp_1024"]["24"] > 0.5
+    _clamp_case(synth.preset("encoder_clamp_1024"), 5, False)
 
 
 def _rotary_case(cfg, prefix, tol):
@@ -88,19 +107,23 @@ def _rotary_case(cfg, prefix, tol):
           flush=True)
     orc = OracleModel(cfg, w)
     r1 = orc.forward(ids, mask, prefix=prefix)
-    r2 = orc.forward(ids, mask, prefix=prefix)
+    r2 = orc.forward(ids, mask, prefix=1)   # its decisions and effects; its logits are out1's
     assert (r1.regrow, r2.regrow) == (True, False)
     check_decisions(d1, r1, cfg)
     check_decisions(d2, r2, cfg)
-    check_logits(f64(out1[:, :prefix]), r1.logits_f64, cfg.dtype,
-                 f"decoder_4096 {cfg.n_layers} layers prefix {prefix}", tol)
+    n = r1.logits_f64.shape[1]
+    check_logits(f64(out1[:, :n]), r1.logits_f64, cfg.dtype,
+                 f"decoder_4096 {cfg.n_layers} layers, positions [0, {n})", tol)
     assert torch.equal(out1.view(torch.int16), out2.view(torch.int16))
     assert gpu_effects(m) == effects_of(r1) + effects_of(r2)
 
 
 def test_decoder_4096_full_width_2_layers():
-    _rotary_case(synth.preset("decoder_4096", n_layers=2), 256, None)
+    """Every one of the 2048 positions: rows [1024, 2048) of the regrown
+    rotary table, rotations at angles up to 2047 rad, and attention over up to
+    2048 keys at head size 128."""
+    _rotary_case(synth.preset("decoder_4096", n_layers=2), None, None)
 
 
 def test_decoder_4096_full_depth():
-    _rotary_case(synth.preset("decoder_4096"), 96, FULL_DEPTH_TOL["decoder_4096"])
+    _rotary_case(synth.preset("decoder_4096"), 96, 2 * SPREAD["decoder_4096"]["32_prefix96"])

@@ -73,6 +73,12 @@ def check_decisions(dec, res, cfg):
         assert dec["clamp"] == flat
         am = [np.float32(v) for pair in res.clamp_absmax for v in pair]
         print("clamp sites", flat, "absmax gpu", dec["clamp_absmax"], "oracle", am)
+        # the NaN flag exactly; the largest magnitude of each site's stored
+        # stream within the logits tolerance (the two forwards' streams differ
+        # by rounding; test_gpu_stepwise compares it exactly on one stream)
+        assert dec["clamp_nan"] == [bool(v) for pair in res.clamp_nan for v in pair]
+        for g, o in zip(dec["clamp_absmax"], am):
+            assert (np.isinf(g) and np.isinf(o)) or abs(g - o) <= TOL[cfg.dtype] * max(abs(o), 1.0)
 
 
 def inputs(cfg, seed, want_pads):
