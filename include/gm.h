@@ -274,6 +274,25 @@ int gm_forward(gm_model *m, const int32_t *token_ids, const int32_t *attn_mask,
 int gm_forward_ex(gm_model *m, int32_t B, int32_t S, const int32_t *token_ids,
                   const int32_t *attn_mask, void *out_logits, hipStream_t stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops, harnesses that forbid hipMalloc): the forward of
+ * gm_forward_ex enqueued directly on `stream`, kernel by kernel (so a
+ * caller's stream capture records it), as one branch, with its activation
+ * workspace (h, a, qkv, ctx, f, and tmp for post-norm models) taken from a
+ * static device array of the library instead of the model's buffers.  It
+ * calls no allocating routine.  Same arguments, results, decisions, effects
+ * and trap behaviour as gm_forward_ex.
+ *  Limit: B * S * (6 * d_model + d_ff) elements of act_dtype (each buffer
+ *  rounded up to 256 bytes; 7 * d_model for post-norm models) must fit in
+ *  the 64 MiB array, else GM_E_INVAL with the sizes in gm_last_error.
+ *  The current device must be the model's device.
+ *  The array is one per device, shared by every call on that device (of
+ *  any model) and it keeps the last call's contents (the forward writes
+ *  every workspace element before reading it): calls that overlap on one
+ *  device race.  Not for encoder-decoder models. */
+int gm_forward_noalloc(gm_model *m, int32_t B, int32_t S, const int32_t *token_ids,
+                       const int32_t *attn_mask, void *out_logits, hipStream_t stream);
+
 /* Paper: Evaluation, "Experimental Setup" (text models generate greedily
  * token by token) and "Throughput Improvement"; the rotary-cache regrow of
  * the Motivation's Phi-4 example fires mid-generation (rule [Where]).

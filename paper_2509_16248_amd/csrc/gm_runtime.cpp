@@ -7,6 +7,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -73,6 +74,31 @@ constexpr int kMaxGraphs = 8;
 
 }  // namespace
 
+// Static device scratch of gm_forward_noalloc (each device holds its own copy
+// for the life of the process).  In host code `scratch` names a host-side
+// stand-in: kernels get the device address from hipGetSymbolAddress, taken
+// once per device at model creation and kept in g_scratch_ptr.
+constexpr size_t kScratchBytes = size_t(64) << 20;
+static __device__ __align__(256) char scratch[kScratchBytes];
+constexpr int kMaxDevices = 64;
+static void* g_scratch_ptr[kMaxDevices] = {};
+static std::mutex g_scratch_mu;
+
+// Device address of this device's scratch array (current device = dev).
+static int scratch_for_device(int dev, void** out) {
+  if (dev < 0 || dev >= kMaxDevices) return inval("device ordinal out of range for the scratch table");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) return hip_fail(e != hipSuccess ? e : hipErrorInvalidSymbol,
+                                               "hipGetSymbolAddress(scratch)");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return GM_OK;
+}
+
 struct gm_model {
   gm_config cfg;
   int device = 0;
@@ -135,6 +161,8 @@ struct gm_model {
   // tensor-valued deferred logs (cfg.log_hidden): per-forward values [L][max_batch]
   // and the arena the effect records point into
   float *log_stage = nullptr, *log_arena = nullptr;
+  // device address of the static scratch array on this model's device
+  void* scratch = nullptr;
 
   int alloc(void** p, size_t bytes) {
     *p = nullptr;
@@ -307,7 +335,8 @@ struct Prof {
 };
 
 // Activation workspace of one forward (h, a, qkv, ctx, f and, post-norm,
-// tmp): the model's own buffers unless a caller supplies others.
+// tmp): the model's own buffers, or carved from the static scratch array of
+// gm_forward_noalloc.
 struct Work {
   void *h = nullptr, *a = nullptr, *qkv = nullptr, *ctx = nullptr, *f = nullptr, *tmp = nullptr;
 };
@@ -1064,6 +1093,8 @@ int gm_model_create(const gm_config* cfg, const gm_weights* w, gm_model** out) {
   };
   hipError_t e = hipGetDevice(&m->device);
   if (e != hipSuccess) return fail(hip_fail(e, "hipGetDevice"));
+  // this device's static scratch (gm_forward_noalloc), once per device
+  if ((rc = scratch_for_device(m->device, &m->scratch))) return fail(rc);
 
   const int d = c.d_model, hd = d / c.n_heads, ff = c.d_ff, V = c.vocab;
   const bool gated = c.ffn != GM_FFN_GELU;
@@ -1539,6 +1570,54 @@ int gm_debug_forward_layers(gm_model* m, int32_t B, int32_t S, const int32_t* id
   m->stats.eager_forwards++;
   if (c.kv_cache) m->cache_B = B;
   enqueue(m, B, S, ids, mask, logits, stream, nullptr, nullptr, nullptr, &d);
+  HIP_TRY(hipGetLastError());
+  return GM_OK;
+}
+
+int gm_forward_noalloc(gm_model* m, int32_t B, int32_t S, const int32_t* ids,
+                       const int32_t* mask, void* logits, hipStream_t stream) {
+  if (!m) return inval("model is NULL");
+  const gm_config& c = m->cfg;
+  if (c.n_dec_layers) return inval("an encoder-decoder model runs gm_forward_seq2seq");
+  if (!ids || !mask || !logits) return inval("ids, mask and logits must be non-NULL");
+  if ((reinterpret_cast<uintptr_t>(ids) | reinterpret_cast<uintptr_t>(mask) |
+       reinterpret_cast<uintptr_t>(logits)) & 15)
+    return inval("ids, mask and logits must be 16-byte aligned");
+  if (B < 1 || B > c.max_batch || S < 1 || S > c.max_seq) return inval("B or S out of range");
+  // workspace: h, a, qkv, ctx, f (and tmp for post-norm models), each
+  // rounded up to 256 bytes, carved from the static scratch array
+  const size_t T = static_cast<size_t>(B) * S, d = c.d_model, es = m->esz;
+  auto up = [](size_t n) { return (n + 255) & ~size_t(255); };
+  const size_t sizes[6] = {T * d * es, T * d * es, T * 3 * d * es, T * d * es,
+                           T * c.d_ff * es, c.norm_place == GM_NORM_POST ? T * d * es : 0};
+  size_t total = 0;
+  for (size_t z : sizes) total += up(z);
+  if (total > kScratchBytes) {
+    g_last_error = "workspace of " + std::to_string(total) + " bytes exceeds the static scratch of " +
+                   std::to_string(kScratchBytes) + " bytes (B * S * (6 d + d_ff) * element size)";
+    return GM_E_INVAL;
+  }
+  int dev = -1;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev != m->device) return inval("the current device is not the model's device");
+  char* base = static_cast<char*>(m->scratch);
+  void* ptrs[6];
+  size_t off = 0;
+  for (int i = 0; i < 6; ++i) {
+    ptrs[i] = sizes[i] ? base + off : nullptr;
+    off += up(sizes[i]);
+  }
+  Work w;
+  w.h = ptrs[0];
+  w.a = ptrs[1];
+  w.qkv = ptrs[2];
+  w.ctx = ptrs[3];
+  w.f = ptrs[4];
+  w.tmp = ptrs[5];
+  m->stats.forwards++;
+  m->stats.eager_forwards++;
+  if (c.kv_cache) m->cache_B = B;
+  enqueue(m, B, S, ids, mask, logits, stream, nullptr, nullptr, nullptr, nullptr, &w);
   HIP_TRY(hipGetLastError());
   return GM_OK;
 }

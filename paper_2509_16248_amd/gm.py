@@ -104,7 +104,7 @@ EXPORTS = ["gm_model_create", "gm_model_destroy", "gm_forward", "gm_forward_ex",
            "gm_decode_step", "gm_set_mask_guard", "gm_trap_info", "gm_forward_seq2seq",
            "gm_profile_forward", "gm_set_exec_mode", "gm_set_graph_mode", "gm_read_decisions", "gm_decisions_device_ptr",
            "gm_check_error", "gm_flush_effects", "gm_debug_buffer", "gm_debug_forward_layers",
-           "gm_get_stats",
+           "gm_get_stats", "gm_forward_noalloc",
            "gm_strerror",
            "gm_last_error"]
 
@@ -126,6 +126,7 @@ def lib(path: str = LIB_PATH) -> ctypes.CDLL:
     L.gm_model_destroy.restype = None
     L.gm_forward.argtypes = [_vp, _vp, _vp, _vp, _vp]
     L.gm_forward_ex.argtypes = [_vp, _i32, _i32, _vp, _vp, _vp, _vp]
+    L.gm_forward_noalloc.argtypes = [_vp, _i32, _i32, _vp, _vp, _vp, _vp]
     L.gm_decode_step.argtypes = [_vp, _i32, _vp, _vp, _vp, _vp]
     L.gm_set_mask_guard.argtypes = [_vp, _vp, _i32, _i32]
     L.gm_forward_seq2seq.argtypes = [_vp, _i32, _i32, _vp, _vp, _i32, _vp, _vp, _vp, _vp]
@@ -285,6 +286,11 @@ def gm_debug_buffer(m: int, which: int):
     p, n = _vp(), _u64()
     _check(lib().gm_debug_buffer(m, which, ctypes.byref(p), ctypes.byref(n)), "gm_debug_buffer")
     return p.value, n.value
+
+
+def gm_forward_noalloc(m: int, B: int, S: int, ids: int, mask: int, logits: int,
+                       stream: int) -> None:
+    _check(lib().gm_forward_noalloc(m, B, S, ids, mask, logits, stream), "gm_forward_noalloc")
 
 
 def gm_debug_forward_layers(m: int, B: int, S: int, ids: int, mask: int, logits: int,

@@ -132,6 +132,18 @@ class GmModel:
                          logits.data_ptr(), self._stream(stream))
         return logits
 
+    def forward_noalloc(self, ids: torch.Tensor, mask: torch.Tensor, logits: torch.Tensor,
+                        stream=None) -> torch.Tensor:
+        """gm_forward_noalloc: the forward with its workspace in the
+        library's static device scratch (no allocation; capturable)."""
+        B, S = ids.shape
+        assert ids.dtype == torch.int32 and mask.dtype == torch.int32
+        assert mask.shape == ids.shape and ids.is_contiguous() and mask.is_contiguous()
+        assert logits.shape == (B, S, self.c.vocab) and logits.is_contiguous()
+        gm.gm_forward_noalloc(self.handle, B, S, ids.data_ptr(), mask.data_ptr(),
+                              logits.data_ptr(), self._stream(stream))
+        return logits
+
     def forward_seq2seq(self, src_ids: torch.Tensor, src_mask: torch.Tensor,
                         tgt_ids: torch.Tensor, tgt_mask: torch.Tensor, logits: torch.Tensor,
                         stream=None) -> torch.Tensor:
