@@ -271,13 +271,19 @@ __device__ __forceinline__ void tile_epilogue(const GemmArgs& a,
   const int l32 = lane & 31, g = lane >> 5;
   __syncthreads();   // every wavefront is done reading operand tiles from smem
   SiteMax sm;
-  if (STAGE && !a.kc && (a.epi == kEpiStore || a.epi == kEpiGelu || a.epi == kEpiResid)) {
-    // Column-independent epilogues finish in registers (bias, then GELU or
-    // the residual, one rounding to the output type, the site statistics
-    // of the rounded values) and stage the tile in LDS in the output type;
-    // rows then leave with consecutive lanes on consecutive columns: 16-byte
-    // chunks when output rows are 16-byte aligned, single elements otherwise
-    // (the odd vocabulary of the head).
+  const bool gated = a.epi == kEpiGatedGelu || a.epi == kEpiGatedSilu;
+  // rotary pairs stay inside the tile when whole heads do
+  const bool rope = a.epi == kEpiRope && BN % a.head_dim == 0;
+  const bool plain = a.epi == kEpiStore || a.epi == kEpiGelu || a.epi == kEpiResid;
+  if (STAGE && !a.kc && (plain || gated || rope)) {
+    // The tile finishes in registers (bias, then GELU, the residual, the
+    // gate product or the rotation; one rounding to the output type; the
+    // site statistics of the rounded values), is staged in LDS in the
+    // output type at its output columns (a gated tile is BN/2 wide; rotated
+    // q/k columns go back to their head positions, which stay inside the
+    // tile), and rows leave with consecutive lanes on consecutive columns:
+    // 16-byte chunks when output rows are 16-byte aligned, single elements
+    // otherwise (the odd vocabulary of the head).
     constexpr int LDB = BN + 8;
     T* stb = reinterpret_cast<T*>(smem);
     const T* bias = static_cast<const T*>(a.bias);
@@ -286,66 +292,146 @@ __device__ __forceinline__ void tile_epilogue(const GemmArgs& a,
     const bool resid = a.epi == kEpiResid;
     const T* res = static_cast<const T*>(a.resid);
     const bool res8 = resid && (a.ldr & 3) == 0 && (reinterpret_cast<uintptr_t>(res) & 7) == 0;
-    static_for<0, TM>([&](auto i) {
-      const int ml = wm * WTM + 32 * i + l32;
-      const int m = bm + ml;
-      static_for<0, TN>([&](auto j) {
-        static_for<0, 4>([&](auto q) {
-          const int nl = wn * WTN + 32 * j + 8 * q + 4 * g;
-          const int n0 = bn + nl;
-          float v[4];
+    auto stage4 = [&](int ml, int col, const float* v) {
+      u32x2 w;
+      T* we = reinterpret_cast<T*>(&w);
 #pragma unroll
-          for (int r = 0; r < 4; ++r) v[r] = acc[i][j][4 * q + r];
-          if (bias) {
-            if (bias8 && n0 + 4 <= a.N) {
-              const u32x2 bb = *reinterpret_cast<const u32x2*>(bias + n0);
-              const T* be = reinterpret_cast<const T*>(&bb);
+      for (int r = 0; r < 4; ++r) we[r] = from_f32<T>(v[r]);
+      *reinterpret_cast<u32x2*>(&stb[ml * LDB + col]) = w;
+    };
+    if (gated) {
+      static_for<0, TM>([&](auto i) {
+        const int ml = wm * WTM + 32 * i + l32;
+        static_for<0, TN>([&](auto j) {
+          static_for<0, 2>([&](auto q) {
+            const int nl = wn * WTN + 32 * j + 8 * q + 4 * g;
+            const int nA = bn + nl;
+            float y[4];
 #pragma unroll
-              for (int r = 0; r < 4; ++r) v[r] += to_f32(be[r]);
-            } else {
-#pragma unroll
-              for (int r = 0; r < 4; ++r)
-                if (n0 + r < a.N) v[r] += to_f32(bias[n0 + r]);
+            for (int r = 0; r < 4; ++r) {
+              float gv = acc[i][j][4 * q + r], u = acc[i][j][4 * (q + 2) + r];
+              if (bias && nA + 16 + r < a.N) {
+                gv += to_f32(bias[nA + r]);
+                u += to_f32(bias[nA + 16 + r]);
+              }
+              const float act = a.epi == kEpiGatedGelu ? gelu_f(gv) : silu_f(gv);
+              y[r] = act * u;
             }
-          }
-          if (a.epi == kEpiGelu)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) v[r] = gelu_f(v[r]);
-          if (resid && m < a.M) {
-            const T* rrow = res + static_cast<long long>(m) * a.ldr + n0;
-            if (res8 && n0 + 4 <= a.N) {
-              const u32x2 rr = *reinterpret_cast<const u32x2*>(rrow);
-              const T* re = reinterpret_cast<const T*>(&rr);
-#pragma unroll
-              for (int r = 0; r < 4; ++r) v[r] += to_f32(re[r]);
-            } else {
-#pragma unroll
-              for (int r = 0; r < 4; ++r)
-                if (n0 + r < a.N) v[r] += to_f32(rrow[r]);
-            }
-          }
-          u32x2 w;
-          T* we = reinterpret_cast<T*>(&w);
-#pragma unroll
-          for (int r = 0; r < 4; ++r) we[r] = from_f32<T>(v[r]);
-          if (resid && a.site >= 0 && m < a.M)
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-              if (n0 + r < a.N) sm.add(to_f32(we[r]));
-          *reinterpret_cast<u32x2*>(&stb[ml * LDB + nl]) = w;
+            stage4(ml, (nl >> 5) * 16 + (nl & 15), y);
+          });
         });
       });
-    });
+    } else if (rope) {
+      const int d = a.d_model, hd = a.head_dim, P = hd >> 1;
+      const long long set = a.rope_set_stride && a.state[kRopeLong] ? a.rope_set_stride : 0;
+      static_for<0, TM>([&](auto i) {
+        const int ml = wm * WTM + 32 * i + l32;
+        const int m = bm + ml;
+        int pos = m < a.M ? (a.pos ? a.pos[m] : m % a.seq) : 0;
+        pos = pos < a.rope_rows ? pos : a.rope_rows - 1;
+        static_for<0, TN>([&](auto j) {
+          static_for<0, 2>([&](auto q) {
+            const int nl = wn * WTN + 32 * j + 8 * q + 4 * g;
+            const int nA = bn + nl;
+            float x1[4], x2[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              x1[r] = acc[i][j][4 * q + r];
+              x2[r] = acc[i][j][4 * (q + 2) + r];
+              if (bias && nA + 16 + r < a.N) {
+                x1[r] += to_f32(bias[nA + r]);
+                x2[r] += to_f32(bias[nA + 16 + r]);
+              }
+            }
+            if (nA < 2 * d) {
+              const int region = nA >= d;
+              const int nr = nA - region * d;
+              const int h = nr / hd, within = nr - h * hd;
+              const int ii = (within >> 5) * 16 + (within & 15);
+              const float* cs = a.rope_cos + set + static_cast<long long>(pos) * P + ii;
+              const float* sn = a.rope_sin + set + static_cast<long long>(pos) * P + ii;
+              float o1[4], o2[4];
+#pragma unroll
+              for (int r = 0; r < 4; ++r) {
+                o1[r] = x1[r] * cs[r] - x2[r] * sn[r];
+                o2[r] = x2[r] * cs[r] + x1[r] * sn[r];
+              }
+              const int col = region * d + h * hd + ii - bn;
+              stage4(ml, col, o1);
+              stage4(ml, col + P, o2);
+            } else {
+              stage4(ml, nl, x1);
+              stage4(ml, nl + 16, x2);
+            }
+          });
+        });
+      });
+    } else {
+      static_for<0, TM>([&](auto i) {
+        const int ml = wm * WTM + 32 * i + l32;
+        const int m = bm + ml;
+        static_for<0, TN>([&](auto j) {
+          static_for<0, 4>([&](auto q) {
+            const int nl = wn * WTN + 32 * j + 8 * q + 4 * g;
+            const int n0 = bn + nl;
+            float v[4];
+  #pragma unroll
+            for (int r = 0; r < 4; ++r) v[r] = acc[i][j][4 * q + r];
+            if (bias) {
+              if (bias8 && n0 + 4 <= a.N) {
+                const u32x2 bb = *reinterpret_cast<const u32x2*>(bias + n0);
+                const T* be = reinterpret_cast<const T*>(&bb);
+  #pragma unroll
+                for (int r = 0; r < 4; ++r) v[r] += to_f32(be[r]);
+              } else {
+  #pragma unroll
+                for (int r = 0; r < 4; ++r)
+                  if (n0 + r < a.N) v[r] += to_f32(bias[n0 + r]);
+              }
+            }
+            if (a.epi == kEpiGelu)
+  #pragma unroll
+              for (int r = 0; r < 4; ++r) v[r] = gelu_f(v[r]);
+            if (resid && m < a.M) {
+              const T* rrow = res + static_cast<long long>(m) * a.ldr + n0;
+              if (res8 && n0 + 4 <= a.N) {
+                const u32x2 rr = *reinterpret_cast<const u32x2*>(rrow);
+                const T* re = reinterpret_cast<const T*>(&rr);
+  #pragma unroll
+                for (int r = 0; r < 4; ++r) v[r] += to_f32(re[r]);
+              } else {
+  #pragma unroll
+                for (int r = 0; r < 4; ++r)
+                  if (n0 + r < a.N) v[r] += to_f32(rrow[r]);
+              }
+            }
+            u32x2 w;
+            T* we = reinterpret_cast<T*>(&w);
+  #pragma unroll
+            for (int r = 0; r < 4; ++r) we[r] = from_f32<T>(v[r]);
+            if (resid && a.site >= 0 && m < a.M)
+  #pragma unroll
+              for (int r = 0; r < 4; ++r)
+                if (n0 + r < a.N) sm.add(to_f32(we[r]));
+            *reinterpret_cast<u32x2*>(&stb[ml * LDB + nl]) = w;
+          });
+        });
+      });
+    }
     __syncthreads();
+    // output tile: OW columns from column ob of rows of a.ldo elements
+    const int OW = gated ? BN / 2 : BN;
+    const int ob = gated ? bn / 2 : bn;
+    const int nout = gated ? a.N / 2 : a.N;
+    const int ncol = nout - ob < OW ? nout - ob : OW;
     if ((a.ldo & 7) == 0) {
-      constexpr int CPR = BN / 8;
-      const int ncol = a.N - bn < BN ? a.N - bn : BN;
-      for (int e = t; e < BM * CPR; e += NT) {
-        const int ml = e / CPR, j0 = 8 * (e % CPR);
+      const int cpr = OW / 8;
+      for (int e = t; e < BM * cpr; e += NT) {
+        const int ml = e / cpr, j0 = 8 * (e % cpr);
         const int m = bm + ml;
         if (m >= a.M || j0 >= ncol) continue;
         const u32x4 w = *reinterpret_cast<const u32x4*>(&stb[ml * LDB + j0]);
-        T* orow = out + static_cast<long long>(m) * a.ldo + bn;
+        T* orow = out + static_cast<long long>(m) * a.ldo + ob;
         if (j0 + 8 <= ncol) {
           *reinterpret_cast<u32x4*>(orow + j0) = w;
         } else {
@@ -356,11 +442,11 @@ __device__ __forceinline__ void tile_epilogue(const GemmArgs& a,
         }
       }
     } else {
-      for (int e = t; e < BM * BN; e += NT) {
-        const int ml = e / BN, nl = e % BN;
-        const int m = bm + ml, n = bn + nl;
-        if (m >= a.M || n >= a.N) continue;
-        out[static_cast<long long>(m) * a.ldo + n] = stb[ml * LDB + nl];
+      for (int e = t; e < BM * OW; e += NT) {
+        const int ml = e / OW, nl = e % OW;
+        const int m = bm + ml;
+        if (m >= a.M || nl >= ncol) continue;
+        out[static_cast<long long>(m) * a.ldo + ob + nl] = stb[ml * LDB + nl];
       }
     }
   } else {
