@@ -426,7 +426,8 @@ def main():
     del m, loaded, out
     torch.cuda.empty_cache()
     roof = head["gemm"]
-    roof["kernel"] = "k_gemm_x (every projection GEMM and the LM head of the forward)"
+    roof["kernel"] = ("k_gemm_big (128x384, 256x256 and 256x128 tiles): every projection GEMM "
+                      "and the LM head of the forward")
     roof["traffic"] = measured_traffic(WORKLOAD)
     roof["timing"] = ("HIP events on the launch stream around each kernel of an eager forward "
                       "that runs the same launches as the graph (batch 1: one branch)")

@@ -794,9 +794,10 @@ template <typename T>
 static void gemm_mfma(const GemmArgs& a, hipStream_t s) {
   // Long products (K >= 2048: the 4096-wide decoder's projections and head)
   // take the large-tile kernel, with the tile that fills the chip best:
-  // 256 x 256 when there are two or more waves of such tiles (256 CUs), a
-  // K step of 64 in two stages at 1.25 - 2 waves, 256 x 128 from one wave
-  // on (O and down at 2048 x 4096).  Measured on those shapes, same bits.
+  // 256 x 256 when there are two or more waves of such tiles (256 CUs),
+  // 128 x 384 when it fills whole waves, a K step of 64 in two stages at
+  // 1.25 - 2 waves, 256 x 128 from one wave on (O and down at 2048 x 4096).
+  // Measured on those shapes, same bits.
   // Shorter K (the 768- and 1024-wide models) stays on 128 x 128 tiles, 8
   // wavefronts of 64 x 32, operands fetched two K steps ahead; products too
   // small to give the chip ~160 such tiles (1024-row decoder GEMMs of an
@@ -807,6 +808,10 @@ static void gemm_mfma(const GemmArgs& a, hipStream_t s) {
   };
   if (a.K >= 2048) {
     if (tiles(256, 256) >= 512) return run_big<T, 256, 256, 2, 4, 32, 4>(a, s);
+    // 128 x 384 when that fills whole waves exactly (QKV 2048 x 12288: 512
+    // tiles, where 256 x 256 gives 1.5 waves): 233 -> 218 us
+    if (tiles(128, 384) % 256 == 0 && a.N % 384 == 0 && a.M % 128 == 0)
+      return run_big<T, 128, 384, 2, 4, 64, 2>(a, s);
     if (tiles(256, 256) >= 320) return run_big<T, 256, 256, 2, 4, 64, 2>(a, s);
     if (tiles(256, 128) >= 224) return run_big<T, 256, 128, 2, 4, 64, 3>(a, s);
   }

@@ -31,13 +31,13 @@ WORKLOADS = {
     "decoder_4096": {
         "kernels": ("void gm::k_gemm_big<", "void gm::k_gemm_x<"),
         # grid size (threads) -> the launch it is, at 1 x 2048 tokens
-        "shapes": {196608: "QKV 2048x12288x4096 (256x256 tiles, BK 64 x 2)",
+        "shapes": {262144: "QKV 2048x12288x4096 (128x384 tiles, BK 64 x 2)",
                    131072: "O 2048x4096x4096 / down 2048x4096x11008 (256x128 tiles)",
                    352256: "gate|up 2048x22016x4096 (256x256 tiles, BK 32 x 4)",
                    512000: "head 2048x32000x4096 (256x256 tiles, BK 32 x 4)"},
         "copy_bytes": 32000 * 4096 * 2,
         "algorithmic": {   # operands read once + output written once (+ residual read)
-            196608: 2 * (2048 * 4096 + 12288 * 4096 + 2048 * 12288),
+            262144: 2 * (2048 * 4096 + 12288 * 4096 + 2048 * 12288),
             131072: None,  # O and down differ; averaged from the two below
             352256: 2 * (2048 * 4096 + 22016 * 4096 + 2048 * 11008),
             512000: 2 * (2048 * 4096 + 32000 * 4096 + 2048 * 32000)},
