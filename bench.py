@@ -402,6 +402,8 @@ def main():
                     help="measure one workload only (one JSON object, no headline)")
     ap.add_argument("--seq2seq-only", action="store_true",
                     help="only the encoder-decoder measurement (one JSON object)")
+    ap.add_argument("--decode-only", action="store_true",
+                    help="only the KV-cache decode measurement (one JSON object)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU (got --gpus {args.gpus}); "
@@ -412,6 +414,9 @@ def main():
 
     if args.seq2seq_only:
         print(json.dumps(seq2seq_bench(args)), flush=True)
+        return
+    if args.decode_only:
+        print(json.dumps(decode_bench()), flush=True)
         return
     if args.only:
         r, _, _, _ = measure(args.only, args, frag=not args.no_fragmented)
