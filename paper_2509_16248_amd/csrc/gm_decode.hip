@@ -130,8 +130,10 @@ void launch_kv_store(const KvArgs& a, hipStream_t s) {
 // [split*chunk, (split+1)*chunk) of sequence b up to its position pos[b]:
 // G = hd/VN lanes hold one key row (16 bytes each), so a wavefront handles
 // 64/G keys per step; each lane group keeps an online softmax (max m, sum l,
-// unnormalised output o over its VN dimensions).  The groups are merged in
-// LDS; with one chunk per head the workgroup normalises and writes the
+// unnormalised output o over its VN dimensions).  16 wavefronts, so that a
+// cache of up to 512 keys (16-bit, head size 64) is one round trip of
+// loads.  The groups of a wavefront are merged by shuffles, the wavefronts
+// in LDS; with one chunk per head the workgroup normalises and writes the
 // context, otherwise the chunk's (m, l, o) goes to the workspace and
 // k_decode_combine merges the chunks.  (A last-workgroup-merges ticket would
 // save that launch but needs a device-scope fence per workgroup, which on
@@ -139,14 +141,15 @@ void launch_kv_store(const KvArgs& a, hipStream_t s) {
 // Keys marked invalid get weight 0; a sequence without a valid key gets a
 // zero context.
 template <typename T, int HD>
-__global__ __launch_bounds__(256) void k_decode_attn(DecAttnArgs a) {
+__global__ __launch_bounds__(1024) void k_decode_attn(DecAttnArgs a) {
+  constexpr int NWV = 16;                      // wavefronts
   constexpr int VN = 16 / static_cast<int>(sizeof(T));
   constexpr int G = HD / VN;
   constexpr int KPW = 64 / G;
-  constexpr int NG = 4 * KPW;                  // lane groups in the workgroup
+  constexpr int NG = NWV * KPW;                // lane groups in the workgroup
   typedef typename std::conditional<sizeof(T) == 4, f32x4v, u32x4>::type V;
-  __shared__ float s_m[NG], s_l[NG];
-  __shared__ float s_o[NG][HD + 1];
+  __shared__ float s_m[NWV], s_l[NWV];
+  __shared__ float s_o[NWV][HD + 1];
   const int bh = blockIdx.x, split = blockIdx.y;
   const int b = bh / a.H, h = bh % a.H;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -171,7 +174,8 @@ __global__ __launch_bounds__(256) void k_decode_attn(DecAttnArgs a) {
 #pragma unroll
   for (int i = 0; i < VN; ++i) o[i] = 0.f;
   // U keys per lane group per trip, their K and V rows loaded up front so
-  // that the loads of U keys are in flight together
+  // that the loads of U keys are in flight together (16 wavefronts: 512
+  // keys per trip at head size 64 in 16-bit)
   constexpr int U = 4;
   for (int j0 = k0 + wave * KPW + grp; j0 < k1; j0 += U * NG) {
     V kr[U], vr[U];
@@ -204,22 +208,36 @@ __global__ __launch_bounds__(256) void k_decode_attn(DecAttnArgs a) {
       m = mn;
     }
   }
-  const int gi = wave * KPW + grp;
-  if (gl == 0) {
-    s_m[gi] = m;
-    s_l[gi] = l;
-  }
+  // merge the wavefront's lane groups (lanes G, 2G, .. apart hold the same
+  // dimensions of other keys), then the wavefronts in LDS
 #pragma unroll
-  for (int i = 0; i < VN; ++i) s_o[gi][gl * VN + i] = o[i];
+  for (int off = G; off < 64; off <<= 1) {
+    const float mo = __shfl_xor(m, off, 64), lo = __shfl_xor(l, off, 64);
+    const float mm = fmaxf(m, mo);
+    const float w0 = m == -INFINITY ? 0.f : expf(m - mm);
+    const float w1 = mo == -INFINITY ? 0.f : expf(mo - mm);
+    l = l * w0 + lo * w1;
+#pragma unroll
+    for (int i = 0; i < VN; ++i) o[i] = o[i] * w0 + __shfl_xor(o[i], off, 64) * w1;
+    m = mm;
+  }
+  if (lane < G) {
+    if (lane == 0) {
+      s_m[wave] = m;
+      s_l[wave] = l;
+    }
+#pragma unroll
+    for (int i = 0; i < VN; ++i) s_o[wave][gl * VN + i] = o[i];
+  }
   __syncthreads();
   float* part = a.part + ((static_cast<long long>(bh) * a.nsplit) + split) * (HD + 2);
   T* ctx = static_cast<T*>(a.ctx) + static_cast<long long>(b) * a.d + h * HD;
   for (int i = threadIdx.x; i < HD; i += blockDim.x) {
     float M = -INFINITY;
-    for (int g2 = 0; g2 < NG; ++g2) M = fmaxf(M, s_m[g2]);
+    for (int g2 = 0; g2 < NWV; ++g2) M = fmaxf(M, s_m[g2]);
     float L = 0.f, O = 0.f;
     if (M != -INFINITY)
-      for (int g2 = 0; g2 < NG; ++g2) {
+      for (int g2 = 0; g2 < NWV; ++g2) {
         if (s_m[g2] == -INFINITY) continue;
         const float w = expf(s_m[g2] - M);
         L += s_l[g2] * w;
@@ -259,7 +277,7 @@ __global__ __launch_bounds__(HD) void k_decode_combine(DecAttnArgs a) {
 
 template <typename T, int HD>
 static void decode_attn_t(const DecAttnArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL((k_decode_attn<T, HD>), dim3(a.B * a.H, a.nsplit), dim3(256), 0, s, a);
+  hipLaunchKernelGGL((k_decode_attn<T, HD>), dim3(a.B * a.H, a.nsplit), dim3(1024), 0, s, a);
   if (a.nsplit > 1)
     hipLaunchKernelGGL((k_decode_combine<T, HD>), dim3(a.B * a.H), dim3(HD), 0, s, a);
 }
