@@ -1054,6 +1054,63 @@ __global__ __launch_bounds__(512) void k_gemm_skinny_ks(GemmArgs a) {
   site_flush(a, sm);
 }
 
+// A few rows (M <= 16) against a wide plain output (the LM head of a
+// decode step): the 2 M N K multiply-adds on the matrix cores instead of
+// the VALU.  Each wavefront computes 16 output columns for every row with
+// v_mfma_f32_16x16x32 (16 weight rows as the A operand, the activation rows
+// padded to 16 as the B operand; lane l supplies row l % 16 and k
+// 8 (l / 16) .. + 7 of each 32-wide k step), 8 k steps of loads in flight,
+// and ends with columns 4 (l / 16) .. + 3 of activation row l % 16.
+template <typename T> struct Mfma16;
+template <> struct Mfma16<bf16_t> {
+  typedef bf16x8 vec;
+  static __device__ __forceinline__ f32x4 run(vec a, vec b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+  }
+};
+template <> struct Mfma16<f16_t> {
+  typedef f16x8 vec;
+  static __device__ __forceinline__ f32x4 run(vec a, vec b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+  }
+};
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_gemm_skinny_mfma(GemmArgs a) {
+  typedef typename Mfma16<T>::vec vec;
+  constexpr int U = 8;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int n0 = (blockIdx.x * 4 + wave) * 16;
+  if (n0 >= a.N) return;                     // no barrier in this kernel
+  const int l16 = lane & 15, kg = lane >> 4;
+  const int n = n0 + l16 < a.N ? n0 + l16 : a.N - 1;
+  const int m = l16 < a.M ? l16 : a.M - 1;
+  const T* wp = static_cast<const T*>(a.W) + static_cast<long long>(n) * a.ldw + 8 * kg;
+  const T* xp = static_cast<const T*>(a.A) + static_cast<long long>(m) * a.lda + 8 * kg;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  int k = 0;
+  for (; k + 32 * U <= a.K; k += 32 * U) {
+    vec wf[U], xf[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      wf[u] = *reinterpret_cast<const vec*>(wp + k + 32 * u);
+      xf[u] = *reinterpret_cast<const vec*>(xp + k + 32 * u);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) acc = Mfma16<T>::run(wf[u], xf[u], acc);
+  }
+  for (; k < a.K; k += 32)
+    acc = Mfma16<T>::run(*reinterpret_cast<const vec*>(wp + k), *reinterpret_cast<const vec*>(xp + k),
+                         acc);
+  SiteMax sm;
+  GemmArgs b = a;
+  b.N = a.N - n0 < 16 ? a.N : n0 + 16;       // the pair columns (+16) lie beyond this wavefront's
+  const float va[4] = {acc[0], acc[1], acc[2], acc[3]};
+  const float vb[4] = {0.f, 0.f, 0.f, 0.f};
+  epi_pair<T>(b, l16, n0 + 4 * kg, va, vb, sm);
+  site_flush(a, sm);
+}
+
 template <typename T>
 static void skinny_ks(const GemmArgs& a, hipStream_t s) {
   const dim3 grid((a.N + 7) / 8), block(512);
@@ -1078,6 +1135,13 @@ static void skinny_t(const GemmArgs& a, hipStream_t s) {
   // the gated and rotary epilogues combine packed rows 16 apart; a wide
   // output (the head) has workgroups enough with 32 rows each, and four rows
   // per wavefront reuse every activation load four times
+  // a wide plain output (the head) in 16-bit on the matrix cores
+  if constexpr (sizeof(T) == 2) {
+    if (a.epi == kEpiStore && !a.bias && a.site < 0 && !a.kc && a.N >= 8192 && a.K % 32 == 0) {
+      hipLaunchKernelGGL((k_gemm_skinny_mfma<T>), dim3((a.N + 63) / 64), dim3(256), 0, s, a);
+      return;
+    }
+  }
   if (a.epi == kEpiGatedGelu || a.epi == kEpiGatedSilu || a.epi == kEpiRope || a.N >= 8192)
     skinny_r<T, 4>(a, s);
   else if (a.M <= 8 && a.N < 2048)     // few row groups: split K across the wavefronts

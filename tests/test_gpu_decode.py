@@ -195,3 +195,16 @@ def test_full_size_causal_lm_768_decode_sampled():
     w = synth.make_weights(cfg, 1234)
     ids, mask = synth.make_inputs(cfg, 9, seq=384, max_pad=100)
     decode_case(cfg, w, ids, mask, 3, cfg.seq, "causal_lm_768 full")
+
+
+def test_decode_long_cache_several_load_trips():
+    """Caches longer than one round trip of the decode attention's loads
+    (512 keys at head size 64 in 16-bit; 8 x 12 heads keep one key chunk per
+    (sequence, head)): 2 layers of the 768-wide model with a reduced
+    vocabulary, prompts of 560-700 positions, three steps."""
+    cfg = synth.preset("causal_lm_768", batch=8, n_layers=2, vocab=1000, seq=704, max_pad=140)
+    w = synth.make_weights(cfg, 21)
+    ids, mask = synth.make_inputs(cfg, 5, seq=700)
+    print("prompt lengths", mask.sum(1).tolist(), flush=True)
+    assert mask.sum(1).max() > 512
+    decode_case(cfg, w, ids, mask, 3, cfg.seq, "causal_lm_768 long cache")
