@@ -154,9 +154,8 @@ __global__ __launch_bounds__(1024) void k_decode_attn(DecAttnArgs a) {
   const int b = bh / a.H, h = bh % a.H;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int grp = lane / G, gl = lane % G;
-  const int last = a.pos[b];
   const int k0 = split * a.chunk;
-  const int k1 = min(k0 + a.chunk, last + 1);
+  const int last = a.pos[b];
 
   float q[VN];
   {
@@ -173,22 +172,31 @@ __global__ __launch_bounds__(1024) void k_decode_attn(DecAttnArgs a) {
   float m = -INFINITY, l = 0.f, o[VN];
 #pragma unroll
   for (int i = 0; i < VN; ++i) o[i] = 0.f;
+  constexpr int U = 4;
   // U keys per lane group per trip, their K and V rows loaded up front so
   // that the loads of U keys are in flight together (16 wavefronts: 512
-  // keys per trip at head size 64 in 16-bit)
-  constexpr int U = 4;
-  for (int j0 = k0 + wave * KPW + grp; j0 < k1; j0 += U * NG) {
-    V kr[U], vr[U];
-    bool ok[U];
+  // keys per trip at head size 64 in 16-bit).  The first trip's rows
+  // are fetched before pos[b] (the end of the keys) is known: their
+  // addresses do not depend on it (rows past the chunk read its first row,
+  // inside the cache either way).
+  const int cap = min(k0 + a.chunk, a.max_seq);
+  const int jb = k0 + wave * KPW + grp;
+  V kr[U], vr[U];
+  uint8_t vl[U];
+  auto fetch = [&](int j0) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int j = j0 + u * NG;
-      ok[u] = j < k1;
-      const int jj = ok[u] ? j : k1 - 1;
+      const int jj = j < cap ? j : k0;
       kr[u] = *reinterpret_cast<const V*>(kc + static_cast<long long>(jj) * HD);
       vr[u] = *reinterpret_cast<const V*>(vc + static_cast<long long>(jj) * HD);
-      ok[u] = ok[u] && valid[jj];
+      vl[u] = valid[jj];
     }
+  };
+  fetch(jb);
+  const int k1 = min(k0 + a.chunk, last + 1);
+  for (int j0 = jb; j0 < k1; j0 += U * NG) {
+    if (j0 != jb) fetch(j0);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const T* ke = reinterpret_cast<const T*>(&kr[u]);
@@ -197,7 +205,7 @@ __global__ __launch_bounds__(1024) void k_decode_attn(DecAttnArgs a) {
       for (int i = 0; i < VN; ++i) s += q[i] * to_f32(ke[i]);
 #pragma unroll
       for (int off = G / 2; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
-      if (!ok[u]) continue;                    // the same for the whole lane group
+      if (!(j0 + u * NG < k1 && vl[u])) continue;   // the same for the whole lane group
       s *= a.scale;
       const float mn = fmaxf(m, s);
       const float corr = expf(m - mn), p = expf(s - mn);
