@@ -288,6 +288,23 @@ __global__ __launch_bounds__(256) void k_rownorm(RowArgs a) {
     if (blockIdx.x == 0 && threadIdx.x == 0) a.state[kClampBase + a.clamp_site] = trip;
   }
   if (row >= a.rows) return;
+  // the norm's gain and bias vectors of this lane, fetched before the row
+  // so that they are in flight with it (not one round trip per vector after
+  // the statistics)
+  typedef typename Vec<T>::type RV;
+  RV graw[MAXV], braw[MAXV];
+  const T* g = static_cast<const T*>(a.g);
+  const T* bb = static_cast<const T*>(a.b);
+  if (a.norm >= 0) {
+#pragma unroll
+    for (int j = 0; j < MAXV; ++j) {
+      const int c = (lane + 64 * j);
+      if (c < nvec) {
+        graw[j] = *reinterpret_cast<const RV*>(g + c * VN);
+        if (bb) braw[j] = *reinterpret_cast<const RV*>(bb + c * VN);
+      }
+    }
+  }
   float v[MAXV][VN];
   T* x = static_cast<T*>(a.x) + static_cast<long long>(row) * d;
   if (a.ids) {
@@ -297,16 +314,25 @@ __global__ __launch_bounds__(256) void k_rownorm(RowArgs a) {
     const int position = a.pos ? a.pos[row] : row % a.seq;
     const T* p = a.pos_emb ? static_cast<const T*>(a.pos_emb) + static_cast<long long>(position) * d
                            : nullptr;
+    // every load of the row first, then the stores (a store between two
+    // loads would make the second wait for it)
+    RV praw[MAXV];
 #pragma unroll
     for (int j = 0; j < MAXV; ++j) {
       const int c = (lane + 64 * j);
       if (c < nvec) {
         vload(e + c * VN, v[j]);
-        if (p) {
-          float q[VN];
-          vload(p + c * VN, q);
+        if (p) praw[j] = *reinterpret_cast<const RV*>(p + c * VN);
+      }
+    }
 #pragma unroll
-          for (int i = 0; i < VN; ++i) v[j][i] += q[i];
+    for (int j = 0; j < MAXV; ++j) {
+      const int c = (lane + 64 * j);
+      if (c < nvec) {
+        if (p) {
+          const T* pe = reinterpret_cast<const T*>(&praw[j]);
+#pragma unroll
+          for (int i = 0; i < VN; ++i) v[j][i] += to_f32(pe[i]);
         }
 #pragma unroll
         for (int i = 0; i < VN; ++i) v[j][i] = round_as<T>(v[j][i]);
@@ -356,18 +382,22 @@ __global__ __launch_bounds__(256) void k_rownorm(RowArgs a) {
   s2 = wave_sum(s2);
   const float rstd = 1.0f / sqrtf(s2 / d + a.eps);
   T* out = static_cast<T*>(a.out) + static_cast<long long>(row) * d;
-  const T* g = static_cast<const T*>(a.g);
-  const T* bb = static_cast<const T*>(a.b);
 #pragma unroll
   for (int j = 0; j < MAXV; ++j) {
     const int c = (lane + 64 * j);
     if (c < nvec) {
       float gv[VN], bv[VN];
-      vload(g + c * VN, gv);
-      if (bb) vload(bb + c * VN, bv);
-      else
+      const T* ge = reinterpret_cast<const T*>(&graw[j]);
+#pragma unroll
+      for (int i = 0; i < VN; ++i) gv[i] = to_f32(ge[i]);
+      if (bb) {
+        const T* be = reinterpret_cast<const T*>(&braw[j]);
+#pragma unroll
+        for (int i = 0; i < VN; ++i) bv[i] = to_f32(be[i]);
+      } else {
 #pragma unroll
         for (int i = 0; i < VN; ++i) bv[i] = 0.f;
+      }
 #pragma unroll
       for (int i = 0; i < VN; ++i) v[j][i] = (v[j][i] - mean) * rstd * gv[i] + bv[i];
       vstore(out + c * VN, v[j]);
