@@ -208,3 +208,16 @@ def test_decode_long_cache_several_load_trips():
     print("prompt lengths", mask.sum(1).tolist(), flush=True)
     assert mask.sum(1).max() > 512
     decode_case(cfg, w, ids, mask, 3, cfg.seq, "causal_lm_768 long cache")
+
+
+@pytest.mark.parametrize("dtype,batch", [("f16", 1), ("bf16", 3)])
+def test_decode_wide_head_on_matrix_cores(dtype, batch):
+    """A vocabulary of 9000 (>= 8192) sends the decode step's head to the
+    matrix-core few-row kernel: fp16 and bf16, one row and three rows (the
+    activation rows padded to 16), a vocabulary that is not a multiple of
+    16 columns."""
+    cfg = synth.reduced("causal_lm_768").replace(vocab=9001, batch=batch, seq=64, max_pad=8,
+                                                 dtype=dtype)
+    w = synth.make_weights(cfg, 31)
+    ids, mask = synth.make_inputs(cfg, 2, seq=56)       # room for the 4 steps in the cache
+    decode_case(cfg, w, ids, mask, 4, cfg.seq, f"causal_lm_768 reduced {dtype} vocab 9001")
