@@ -794,10 +794,12 @@ template <typename T>
 static void gemm_mfma(const GemmArgs& a, hipStream_t s) {
   // Long products (K >= 2048: the 4096-wide decoder's projections and head)
   // take the large-tile kernel, with the tile that fills the chip best:
-  // 256 x 256 when there are two or more waves of such tiles (256 CUs),
-  // 128 x 384 when it fills whole waves, a K step of 64 in two stages at
-  // 1.25 - 2 waves, 256 x 128 from one wave on (O and down at 2048 x 4096).
-  // Measured on those shapes, same bits.
+  // 128 x 384 when it fills whole waves (QKV), 256 x 256 from 1.25 waves of
+  // such tiles (256 CUs; gate/up, head), 256 x 128 from one wave on (O and
+  // down at 2048 x 4096).  The 256 x 256 tile takes a K step of 64 in two
+  // stages: against a step of 32 in four, gate/up 357 -> 340 us and the
+  // head 497 -> 465 us (one barrier per 32 MFMAs of a wavefront instead of
+  // 16).  Measured on those shapes, same bits.
   // Shorter K (the 768- and 1024-wide models) stays on 128 x 128 tiles, 8
   // wavefronts of 64 x 32, operands fetched two K steps ahead; products too
   // small to give the chip ~160 such tiles (1024-row decoder GEMMs of an
@@ -807,7 +809,6 @@ static void gemm_mfma(const GemmArgs& a, hipStream_t s) {
     return ((a.M + bm - 1) / bm) * static_cast<long long>((a.N + bn - 1) / bn);
   };
   if (a.K >= 2048) {
-    if (tiles(256, 256) >= 512) return run_big<T, 256, 256, 2, 4, 32, 4>(a, s);
     // 128 x 384 when that fills whole waves exactly (QKV 2048 x 12288: 512
     // tiles, where 256 x 256 gives 1.5 waves): 233 -> 218 us
     if (tiles(128, 384) % 256 == 0 && a.N % 384 == 0 && a.M % 128 == 0)

@@ -2,9 +2,9 @@
 every kernel libgm can launch runs under a test:
 
 * the large-tile GEMM in fp16 (128x384, 256x128 and 256x256 tiles: a
-  one-layer fp16 model of the 4096-wide decoder's shape) and its
-  256x256 tile with a K step of 64 in two stages (a 2048-wide model, whose
-  gate/up product has 352 tiles of 256x256), in bf16 and fp16;
+  one-layer fp16 model of the 4096-wide decoder's shape), and a 2048-wide
+  model whose products take other tile choices (gate/up: 352 tiles of
+  256x256), in bf16 and fp16;
 * attention of 16-bit models with head size 32 (the row kernel);
 * the GM_DEBUG_SYNC switch (one host synchronisation per forward, same
   results).
@@ -37,14 +37,14 @@ def _compare(cfg, seed=3):
 
 def test_large_tile_gemm_fp16():
     """QKV 2048x12288x4096 (128x384 tiles, rotary), O and down (256x128),
-    gate/up and head (256x256, K step 32 in four stages), in fp16."""
+    gate/up and head (256x256, K step 64 in two stages), in fp16."""
     _compare(synth.preset("decoder_4096", n_layers=1, dtype="f16"))
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f16"])
 def test_large_tile_gemm_k64_two_stages(dtype):
     """d 2048, SwiGLU 5632: gate/up 2048x11264x2048 gives 352 tiles of
-    256x256 (K step 64 in two stages); QKV 2048x6144 takes 128x384."""
+    256x256 (1.375 waves); QKV 2048x6144 takes 128x384; K of 2048."""
     cfg = synth.preset("decoder_4096", n_layers=1, d_model=2048, n_heads=16, d_ff=5632,
                        dtype=dtype)
     _compare(cfg)
