@@ -170,7 +170,8 @@ class OracleModel:
     def forward(self, ids: np.ndarray, mask: np.ndarray,
                 force: Optional[Dict] = None,
                 rows: Optional[List[int]] = None,
-                prefix: Optional[int] = None) -> OracleResult:
+                prefix: Optional[int] = None,
+                progress=None) -> OracleResult:
         """Run the original (graph-breaking) forward.
 
         ``force`` overrides the value a host-side predicate reads
@@ -184,7 +185,9 @@ class OracleModel:
         positions of each sequence; with a causal mask they depend on no later
         position, so they equal those positions of the full forward.  The
         predicates (padding branch, rotary cache size) still read the full
-        inputs, as the original program does.
+        inputs, as the original program does.  ``progress``, if given, is
+        called with the layer index after each layer (long runs report
+        progress through it; it takes no part in the arithmetic).
         """
         c = self.cfg
         st = self.begin(ids, mask, force, rows, prefix)
@@ -224,6 +227,8 @@ class OracleModel:
             absmaxes.append((site_out[0][1], site_out[1][1]))
             nans.append((site_out[0][2], site_out[1][2]))
             margins.append((site_out[0][3], site_out[1][3]))
+            if progress is not None:
+                progress(l)
 
         # --- head.
         logits = self.step_head(h)

@@ -11,7 +11,8 @@ expected to agree with it more closely than this.  The end-to-end GPU logits
 tests take twice this spread as their tolerance where it exceeds 1e-2, and
 the per-step tests (test_gpu_stepwise.py) check every layer at 2e-2.
 
-    python tests/golden/depth_spread.py   (repository root; calls only oracle/ and synth/)
+    python tests/golden/depth_spread.py [workload/key]   (repository root;
+    calls only oracle/ and synth/; with an argument, recomputes that entry only)
 """
 import json
 import os
@@ -41,27 +42,42 @@ class Float32Oracle(OracleModel):
         return nx.round_to(x, self.dt).astype(np.float32)
 
 
-def spread(name, n_layers, wseed, iseed, prefix=None):
+def spread(name, n_layers, wseed, iseed):
     cfg = synth.preset(name, n_layers=n_layers)
     w = synth.make_weights(cfg, wseed)
     ids, mask = synth.make_inputs(cfg, iseed)
-    ref = OracleModel(cfg, w).forward(ids, mask, prefix=prefix).logits_f64
-    lo = Float32Oracle(cfg, w).forward(ids, mask, prefix=prefix).logits_f64
+    ref = OracleModel(cfg, w).forward(ids, mask).logits_f64
+    lo = Float32Oracle(cfg, w).forward(ids, mask).logits_f64
     fin = np.isfinite(ref) & np.isfinite(lo)
     return float(np.abs(lo[fin] - ref[fin]).max() / np.abs(ref[fin]).max())
 
 
-def main():
-    out = {"encoder_clamp_1024": {}, "decoder_4096": {}}
-    for L in (2, 4, 8, 24):
-        out["encoder_clamp_1024"][str(L)] = spread("encoder_clamp_1024", L, 5, 0)
-        print("encoder_clamp_1024", L, out["encoder_clamp_1024"][str(L)], flush=True)
-    out["decoder_4096"]["32_prefix96"] = spread("decoder_4096", 32, 11, 0, prefix=96)
-    print("decoder_4096 32 prefix 96", out["decoder_4096"]["32_prefix96"], flush=True)
+ENTRIES = {
+    ("encoder_clamp_1024", "2"): lambda: spread("encoder_clamp_1024", 2, 5, 0),
+    ("encoder_clamp_1024", "4"): lambda: spread("encoder_clamp_1024", 4, 5, 0),
+    ("encoder_clamp_1024", "8"): lambda: spread("encoder_clamp_1024", 8, 5, 0),
+    ("encoder_clamp_1024", "24"): lambda: spread("encoder_clamp_1024", 24, 5, 0),
+    # every one of the 2048 positions at full depth
+    ("decoder_4096", "32_all"): lambda: spread("decoder_4096", 32, 11, 0),
+}
+
+
+def main(only=None):
+    """Recompute every entry, or (only = "workload/key") one of them, and
+    write depth_spread.json."""
     path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "depth_spread.json")
+    out = {"encoder_clamp_1024": {}, "decoder_4096": {}}
+    if only and os.path.exists(path):
+        with open(path) as fh:
+            out.update(json.load(fh))
+    for (w, k), fn in ENTRIES.items():
+        if only and f"{w}/{k}" != only:
+            continue
+        out[w][k] = fn()
+        print(w, k, out[w][k], flush=True)
     with open(path, "w") as fh:
         json.dump(out, fh, indent=1)
 
 
 if __name__ == "__main__":
-    main()
+    main(sys.argv[1] if len(sys.argv) > 1 else None)
