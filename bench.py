@@ -431,7 +431,7 @@ def main():
     del m, loaded, out
     torch.cuda.empty_cache()
     roof = head["gemm"]
-    roof["kernel"] = ("k_gemm_big (128x384, 256x256 and 256x128 tiles): every projection GEMM "
+    roof["kernel"] = ("k_gemm_big (128x384, 256x256 and 128x256 tiles): every projection GEMM "
                       "and the LM head of the forward")
     roof["traffic"] = measured_traffic(WORKLOAD)
     roof["timing"] = ("HIP events on the launch stream around each kernel of an eager forward "

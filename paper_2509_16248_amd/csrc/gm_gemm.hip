@@ -597,8 +597,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm_x(GemmArgs a) {
 }
 
 // ------------------------------------------------------------ large-tile kernel
-// For products with enough tiles of 256 x 256 (or 256 x 128): 8 wavefronts
-// of 128 x 64 (WGM x WGN = 2 x 4) on v_mfma_f32_32x32x16, the same operand
+// For products with enough tiles of 256 x 256 (or 128 x 384, 128 x 256): 8
+// wavefronts (WGM x WGN = 2 x 4) of 128 x 64 (64 x 96, 64 x 64) on
+// v_mfma_f32_32x32x16, the same operand
 // roles, k order and epilogue as k_gemm_x, so the results are the same bits.
 // A wavefront tile of 128 x 64 reads 6 KB of LDS per 8 MFMAs (the 64 x 32
 // tile of k_gemm_x reads 3 KB per 2), and a 256 x 256 workgroup tile loads
@@ -795,11 +796,13 @@ static void gemm_mfma(const GemmArgs& a, hipStream_t s) {
   // Long products (K >= 2048: the 4096-wide decoder's projections and head)
   // take the large-tile kernel, with the tile that fills the chip best:
   // 128 x 384 when it fills whole waves (QKV), 256 x 256 from 1.25 waves of
-  // such tiles (256 CUs; gate/up, head), 256 x 128 from one wave on (O and
-  // down at 2048 x 4096).  The 256 x 256 tile takes a K step of 64 in two
-  // stages: against a step of 32 in four, gate/up 357 -> 340 us and the
-  // head 497 -> 465 us (one barrier per 32 MFMAs of a wavefront instead of
-  // 16).  Measured on those shapes, same bits.
+  // such tiles (256 CUs; gate/up, head), 128 x 256 from one wave on (O and
+  // down at 2048 x 4096).  The 128 x 256 tile gives each wavefront 64 x 64
+  // (4 fragment reads per 4 MFMAs; 256 x 128 gave it 128 x 32, 5 reads):
+  // O 76.6 -> 73.8 us, down 184 -> 177 us.  The 256 x 256 tile takes a K
+  // step of 64 in two stages: against a step of 32 in four, gate/up 357 ->
+  // 340 us and the head 497 -> 465 us (one barrier per 32 MFMAs of a
+  // wavefront instead of 16).  Measured on those shapes, same bits.
   // Shorter K (the 768- and 1024-wide models) stays on 128 x 128 tiles, 8
   // wavefronts of 64 x 32, operands fetched two K steps ahead; products too
   // small to give the chip ~160 such tiles (1024-row decoder GEMMs of an
@@ -814,7 +817,7 @@ static void gemm_mfma(const GemmArgs& a, hipStream_t s) {
     if (tiles(128, 384) % 256 == 0 && a.N % 384 == 0 && a.M % 128 == 0)
       return run_big<T, 128, 384, 2, 4, 64, 2>(a, s);
     if (tiles(256, 256) >= 320) return run_big<T, 256, 256, 2, 4, 64, 2>(a, s);
-    if (tiles(256, 128) >= 224) return run_big<T, 256, 128, 2, 4, 64, 3>(a, s);
+    if (tiles(128, 256) >= 224) return run_big<T, 128, 256, 2, 4, 64, 3>(a, s);
   }
   if (tiles(128, 128) < 160) run_x<T, 64, 64, 2, 2, 2>(a, s);
   else run_x<T, 128, 128, 2, 4, 2>(a, s);

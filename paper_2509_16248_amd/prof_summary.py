@@ -32,7 +32,7 @@ WORKLOADS = {
         "kernels": ("void gm::k_gemm_big<", "void gm::k_gemm_x<"),
         # grid size (threads) -> the launch it is, at 1 x 2048 tokens
         "shapes": {262144: "QKV 2048x12288x4096 (128x384 tiles, BK 64 x 2)",
-                   131072: "O 2048x4096x4096 / down 2048x4096x11008 (256x128 tiles)",
+                   131072: "O 2048x4096x4096 / down 2048x4096x11008 (128x256 tiles)",
                    352256: "gate|up 2048x22016x4096 (256x256 tiles, BK 64 x 2)",
                    512000: "head 2048x32000x4096 (256x256 tiles, BK 64 x 2)"},
         "copy_bytes": 32000 * 4096 * 2,

@@ -1,7 +1,7 @@
 """GPU parity for the kernel paths the five workloads do not reach, so that
 every kernel libgm can launch runs under a test:
 
-* the large-tile GEMM in fp16 (128x384, 256x128 and 256x256 tiles: a
+* the large-tile GEMM in fp16 (128x384, 128x256 and 256x256 tiles: a
   one-layer fp16 model of the 4096-wide decoder's shape), and a 2048-wide
   model whose products take other tile choices (gate/up: 352 tiles of
   256x256), in bf16 and fp16;
@@ -36,7 +36,7 @@ def _compare(cfg, seed=3):
 
 
 def test_large_tile_gemm_fp16():
-    """QKV 2048x12288x4096 (128x384 tiles, rotary), O and down (256x128),
+    """QKV 2048x12288x4096 (128x384 tiles, rotary), O and down (128x256),
     gate/up and head (256x256, K step 64 in two stages), in fp16."""
     _compare(synth.preset("decoder_4096", n_layers=1, dtype="f16"))
 
