@@ -6,6 +6,8 @@ every kernel libgm can launch runs under a test:
   model whose products take other tile choices (gate/up: 352 tiles of
   256x256), in bf16 and fp16;
 * attention of 16-bit models with head size 32 (the row kernel);
+* causal attention with key lengths cut short by long padding, in bf16
+  and fp16;
 * the GM_DEBUG_SYNC switch (one host synchronisation per forward, same
   results).
 
@@ -56,6 +58,23 @@ def test_attention_rows_16bit_head_size_32(dtype):
     kernel for head sizes the MFMA kernel does not cover; with padding."""
     cfg = synth.reduced("causal_lm_768").replace(n_heads=24, dtype=dtype)
     _compare(cfg)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+def test_causal_attention_with_long_padding(dtype):
+    """4 x 512 causal positions with up to 480 trailing pads: key lengths
+    from 32 up, so query blocks past a sequence's last key read no key tile
+    beyond it, and whole key tiles of other blocks are padding."""
+    cfg = synth.reduced("causal_lm_768").replace(seq=512, batch=4, max_pad=480, dtype=dtype)
+    w = synth.make_weights(cfg, 5)
+    ids, mask = synth.make_inputs(cfg, 2)
+    print("pads per sequence", (mask == 0).sum(1).tolist(), flush=True)
+    m = gpu_model(cfg, w)
+    out = run(m, ids, mask)
+    res = OracleModel(cfg, w).forward(ids, mask)
+    check_decisions(m.decisions(), res, cfg)
+    check_logits(f64(out), res.logits_f64, cfg.dtype, f"causal attention, long padding, {dtype}")
+    m.close()
 
 
 def test_debug_sync_switch(monkeypatch):
