@@ -61,7 +61,11 @@ __device__ __forceinline__ void store4(T* p, const float* v, int nvalid, bool ve
 __device__ __forceinline__ float gelu_f(float x) {
   return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f));
 }
-__device__ __forceinline__ float silu_f(float x) { return x / (1.0f + expf(-x)); }
+// x * sigmoid(x) from the hardware exponential and reciprocal (v_exp_f32,
+// v_rcp_f32, about 1 ulp each): x -> -inf gives 1/inf = 0, x -> +inf gives x
+__device__ __forceinline__ float silu_f(float x) {
+  return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(x * -1.4426950408889634f));
+}
 
 struct SiteMax {
   uint32_t amax = 0;
