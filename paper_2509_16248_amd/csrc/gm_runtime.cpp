@@ -671,6 +671,11 @@ void enqueue(gm_model* m, int B, int S, const int32_t* ids, const int32_t* mask,
   int parts = m->split_parts < B ? m->split_parts : B;
   // (a decode step's parts run the skinny kernels, so any part size goes)
   while (!dec && parts > 1 && (B / parts) * S <= 16) --parts;
+  // Models whose projections take the large-tile GEMM (d >= 2048) run a
+  // forward as one branch: a part's products have fewer large tiles than the
+  // chip has CUs (2 x 1024 positions of the 4096-wide decoder: 30.2 ms per
+  // forward as two branches, 28.05 ms as one).
+  if (!dec && d >= 2048) parts = 1;
   if (prof || dump || work || c.fp16_clamp || c.log_hidden || (c.kv_cache && !dec)) parts = 1;
   head_joined = parts > 1 && dec;
   if (parts > 1) {
